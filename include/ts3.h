@@ -1,0 +1,170 @@
+/*
+ * ts3.h -- C ABI of the Transolver-3 Physics-Attention layer on MI355X (gfx950).
+ *
+ * One layer maps point features x [N, C] to x_out [N, C] (paper section 3):
+ *   w     = Softmax_per_head(Linear2(x) / tau)          slice weights, Eq. (1)
+ *   s_raw = w^T x,  d = sum_i w_i                        accumulated over tiles, Eq. (4)
+ *   s     = Linear1(d^-1 s_raw)                          physical states, Eq. (3) / Algorithm 1
+ *   s'    = Attention(s)                                 per head, among its M tokens
+ *   Z     = Linear3(s')  (no bias)                       cached state s'_out, section 3.3
+ *   x_out = w Z + b3                                     full-mesh decoding, Eq. (5)
+ * H heads each own M slices (H*M slice tokens) and a dh = C/H wide block of
+ * Linear1's outputs / Linear3's inputs; attention runs per head with scale
+ * 1/sqrt(dh).  Pass 1 (accumulate) streams tiles of x into an opaque state;
+ * finalize + attention build the cached state Z; pass 2 (deslice) decodes any
+ * chunk of points against it.  The slice weights w are recomputed in pass 2
+ * (Eq. (5)) and never stored.
+ *
+ * Conventions shared by every entry point:
+ *  - Pointers named x, out and every ts3_weights member are DEVICE pointers;
+ *    host_dst / host_src are HOST pointers.  The caller owns all of them; they
+ *    must stay valid until the work enqueued on `stream` has finished.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).  Every
+ *    call only enqueues work and returns; ts3_state_create, ts3_state_free,
+ *    ts3_state_get and ts3_state_set synchronise.
+ *  - Layouts are row-major.  x and out are [n, C] of the state's io dtype
+ *    (float32 or bfloat16, 16-byte aligned); weights are float32.
+ *  - Every call returns a ts3_status; nothing throws or aborts.  On failure the
+ *    state is unchanged unless stated, and ts3_last_error() (per thread)
+ *    describes the cause.  A fault inside an enqueued kernel surfaces as
+ *    TS3_ERR_HIP from a later synchronising call.
+ */
+#ifndef TS3_H
+#define TS3_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    TS3_OK = 0,
+    TS3_ERR_INVALID_ARG = 1,   /* null pointer, bad size, overlapping or misaligned tile */
+    TS3_ERR_BAD_STATE = 2,     /* call out of order (see the state machine below) */
+    TS3_ERR_OUT_OF_MEMORY = 3, /* device allocation failed */
+    TS3_ERR_HIP = 4,           /* a HIP runtime call failed */
+    TS3_ERR_UNSUPPORTED = 5    /* shape this build has no kernel for */
+} ts3_status;
+
+typedef enum { TS3_FP32 = 0, TS3_BF16 = 1 } ts3_dtype;
+
+/* Layer shape and numerics.
+ *  C, H, M, dh : channels, heads, slices per head, head width; H*dh == C.
+ *                Supported: (C, M) in {(64,16), (64,32), (128,16), (128,32),
+ *                (128,64)}, dh == 16; otherwise TS3_ERR_UNSUPPORTED.
+ *  temperature : tau > 0 of the slice softmax; +inf gives uniform weights.
+ *  eps         : added to d before the division in finalize (the paper uses 0).
+ *                A slice with d + eps <= 0 has a zero mean state.
+ *  io_dtype    : ts3_dtype of x and out.  TS3_BF16 stores bf16 and computes
+ *                the slice-weight and contraction products on bf16 matrix
+ *                cores with float32 accumulation; TS3_FP32 uses float32
+ *                matrix cores throughout.
+ *  group_span  : Q, points per accumulation span (> 0, multiple of 32).  Pass 1
+ *                reduces each span to one partial and sums spans in index
+ *                order, so results do not depend on how the mesh is tiled.
+ *  max_points  : largest point index + 1 the state will accumulate; sizes the
+ *                span partials (ceil(max_points / Q) * H * M * (C+1) floats). */
+typedef struct {
+    int32_t C, H, M, dh;
+    float temperature;
+    float eps;
+    int32_t io_dtype;
+    int32_t reserved;
+    int64_t group_span;
+    int64_t max_points;
+} ts3_desc;
+
+/* Layer weights: device pointers to row-major float32.
+ *  W2 [C, H*M], b2 [H*M]   Linear2 -> slice logits; columns h*M..h*M+M-1 are head h
+ *  W1 [C, H*dh], b1 [H*dh] Linear1, applied to the slice tokens
+ *  Wq, Wk, Wv [H, dh, dh]  per-head token-attention projections (no bias)
+ *  W3 [H*dh, C], b3 [C]    Linear3, applied to the slice tokens; b3 added per point
+ * Biases may be NULL (zero). */
+typedef struct {
+    const float *W2, *b2;
+    const float *W1, *b1;
+    const float *Wq, *Wk, *Wv;
+    const float *W3, *b3;
+} ts3_weights;
+
+typedef struct ts3_state ts3_state; /* opaque */
+
+/* Which buffer ts3_state_get / ts3_state_set address (float32, row-major). */
+typedef enum {
+    TS3_S_RAW = 0, /* [H, M, C]  sum_i w_i x_i            (valid after finalize) */
+    TS3_D = 1,     /* [H, M]     sum_i w_i                (valid after finalize) */
+    TS3_S = 2,     /* [H, M, dh] Linear1(d^-1 s_raw)      (valid after finalize) */
+    TS3_S1 = 3,    /* [H, M, dh] Attention(s)             (valid after attention) */
+    TS3_ZP = 4     /* [H, M, C]  Linear3(s'), the cache   (valid after attention) */
+} ts3_buffer;
+
+/* Allocate a state for one layer (device memory on the current HIP device) and
+ * leave it reset.  *out receives the handle; it is NULL on failure. */
+ts3_status ts3_state_create(const ts3_desc *desc, ts3_state **out);
+
+/* Synchronise the device and release the state.  NULL is a no-op. */
+ts3_status ts3_state_free(ts3_state *st);
+
+/* Device bytes the state holds (for peak-memory reports). */
+ts3_status ts3_state_bytes(const ts3_state *st, int64_t *bytes);
+
+/* Begin a new mesh: forget every accumulated tile.  Enqueues nothing. */
+ts3_status ts3_state_reset(ts3_state *st, void *stream);
+
+/* Pass 1 on one geometry tile (Eq. (4), Algorithm 1 tile loop): points
+ * [point_offset, point_offset + n_tile) of the mesh, x_tile -> [n_tile, C].
+ * point_offset must be a multiple of group_span; a tile whose end is not a
+ * multiple of group_span must be the one holding the mesh's last point (no
+ * later tile may start inside its last span); tiles must not overlap; the end
+ * must not pass max_points.  Tiles may arrive in any order.  n_tile == 0 is a
+ * no-op.  The first accumulate after reset records W2/b2 (converted once to
+ * the kernel's operand format); later accumulate and deslice calls must pass
+ * the same W2 and b2 pointers.  State: RESET/ACCUMULATING -> ACCUMULATING. */
+ts3_status ts3_slice_accumulate(ts3_state *st, const ts3_weights *w, const void *x_tile,
+                                int64_t n_tile, int64_t point_offset, void *stream);
+
+/* Sum the span partials in index order into s_raw and d (Eq. (4)) and form
+ * s = Linear1(d^-1 s_raw) per head (Algorithm 1 after the tile loop).
+ * Needs W1 (b1 optional).  State: ACCUMULATING -> FINALIZED. */
+ts3_status ts3_slice_finalize(ts3_state *st, const ts3_weights *w, void *stream);
+
+/* s' = Attention(s) per head, then Z = Linear3(s') (the cached physical state
+ * s'_out of section 3.3), stored with b3 for decoding.  Needs Wq, Wk, Wv, W3
+ * (b3 optional).  State: FINALIZED -> ATTENDED. */
+ts3_status ts3_token_attention(ts3_state *st, const ts3_weights *w, void *stream);
+
+/* Pass 2 on one chunk (Eq. (5), Algorithm 1 deslice loop):
+ * out_chunk[i] = Softmax_per_head(Linear2(x_chunk[i]) / tau) . Z + b3 for
+ * i < n_chunk.  Any chunk, any number of times, any points (not only those
+ * accumulated).  W2/b2 must be the pointers recorded by accumulate.
+ * n_chunk == 0 is a no-op.  State: ATTENDED. */
+ts3_status ts3_deslice(const ts3_state *st, const ts3_weights *w, const void *x_chunk,
+                       int64_t n_chunk, void *out_chunk, void *stream);
+
+/* Whole layer on a resident mesh (Algorithm 1): reset, accumulate tiles of
+ * `tile` points, finalize, attention, deslice chunks of `chunk` points.
+ * tile must be a multiple of group_span; N <= max_points.  Allocates nothing.
+ * Leaves the state ATTENDED. */
+ts3_status ts3_layer_forward(ts3_state *st, const ts3_weights *w, const void *x, int64_t N,
+                             int64_t tile, int64_t chunk, void *out, void *stream);
+
+/* Copy a state buffer to host memory (n floats, must equal its size) after
+ * synchronising `stream`.  For tests and inspection. */
+ts3_status ts3_state_get(const ts3_state *st, int32_t which, float *host_dst, int64_t n,
+                         void *stream);
+
+/* Test hook: overwrite the cached state Z (which == TS3_ZP) and b3 from host
+ * memory (b3 may be NULL = zero), convert it to the decoding operand format,
+ * and mark the state ATTENDED, so pass 2 can be checked on its own.  The W2/b2
+ * pointers used by deslice are taken from `w`.  Synchronises `stream`. */
+ts3_status ts3_state_set(ts3_state *st, const ts3_weights *w, int32_t which,
+                         const float *host_src, int64_t n, const float *host_b3, void *stream);
+
+const char *ts3_status_string(ts3_status s);
+const char *ts3_last_error(void); /* thread-local detail of the last failure */
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TS3_H */

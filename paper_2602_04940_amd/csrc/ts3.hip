@@ -1,0 +1,479 @@
+// Host side of the C ABI declared in include/ts3.h: validation, the state
+// object and its device buffers, the call-order state machine, and kernel
+// dispatch over the supported (dtype, C, M) shapes.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/ts3.h"
+#include "ts3_pass1.h"
+#include "ts3_pass2.h"
+#include "ts3_small.h"
+
+using namespace ts3;
+
+namespace {
+
+thread_local std::string g_err;
+
+ts3_status fail(ts3_status s, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+ts3_status fail(ts3_status s, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return s;
+}
+
+#define HIP_TRY(expr)                                                                          \
+    do {                                                                                       \
+        hipError_t e_ = (expr);                                                                \
+        if (e_ != hipSuccess)                                                                  \
+            return fail(e_ == hipErrorOutOfMemory ? TS3_ERR_OUT_OF_MEMORY : TS3_ERR_HIP,       \
+                        "%s failed: %s", #expr, hipGetErrorString(e_));                        \
+    } while (0)
+
+#define LAUNCH_CHECK(what)                                                                     \
+    do {                                                                                       \
+        hipError_t e_ = hipGetLastError();                                                     \
+        if (e_ != hipSuccess) return fail(TS3_ERR_HIP, "%s launch: %s", what, hipGetErrorString(e_)); \
+    } while (0)
+
+constexpr int ATTN_LDS_MAX = 160 * 1024;
+
+enum Phase { PH_RESET = 0, PH_ACCUM = 1, PH_FINAL = 2, PH_ATTEND = 3 };
+
+// Kernel entry points for one (dtype, C, M) instantiation.
+struct Kernels {
+    void (*pass1)(const void *, int64_t, int64_t, int32_t, int32_t, int32_t, const void *, const float *,
+                  float *, hipStream_t);
+    void (*pass2)(const void *, int64_t, int32_t, const void *, const float *, const void *,
+                  const float *, void *, hipStream_t);
+};
+
+template <typename T, int C, int M>
+void launch_pass1(const void *x, int64_t n, int64_t span0, int32_t Q, int32_t nspan, int32_t H,
+                  const void *w2p, const float *b2s, float *partials, hipStream_t st) {
+    hipLaunchKernelGGL((k_slice_accumulate<T, C, M>), dim3(nspan * H), dim3(256), 0, st,
+                       (const T *)x, n, span0, Q, nspan, H, (const T *)w2p, b2s, partials);
+}
+
+template <typename T, int C, int M>
+void launch_pass2(const void *x, int64_t n, int32_t H, const void *w2p, const float *b2s,
+                  const void *zp, const float *b3, void *out, hipStream_t st) {
+    using Cfg = Pass2Cfg<T, C, M>;
+    const int64_t grid = (n + Cfg::POINTS_PER_WG - 1) / Cfg::POINTS_PER_WG;
+    hipLaunchKernelGGL((k_deslice<T, C, M>), dim3((unsigned)grid), dim3(256), 0, st, (const T *)x, n, H,
+                       (const T *)w2p, b2s, (const T *)zp, b3, (T *)out);
+}
+
+template <typename T, int C, int M> Kernels make_kernels() {
+    return Kernels{&launch_pass1<T, C, M>, &launch_pass2<T, C, M>};
+}
+
+bool find_kernels(int dtype, int C, int M, Kernels *k) {
+#define TS3_SHAPE(CC, MM)                                                                      \
+    if (C == CC && M == MM) {                                                                  \
+        *k = dtype == TS3_BF16 ? make_kernels<bf16_t, CC, MM>() : make_kernels<float, CC, MM>(); \
+        return true;                                                                           \
+    }
+    TS3_SHAPE(64, 16)
+    TS3_SHAPE(64, 32)
+    TS3_SHAPE(128, 16)
+    TS3_SHAPE(128, 32)
+    TS3_SHAPE(128, 64)
+#undef TS3_SHAPE
+    return false;
+}
+
+}  // namespace
+
+struct ts3_state {
+    ts3_desc desc;
+    Kernels k;
+    int esize;          // bytes per io element
+    int64_t nspan_max;  // spans the partial buffer holds
+    int64_t E;          // floats per (span, head-block) partial row group: H*M*(C+1)
+    int64_t nrun_max;
+    // device buffers
+    float *partials = nullptr, *runs = nullptr, *s_raw = nullptr, *dsum = nullptr, *s = nullptr,
+          *s1 = nullptr, *Z = nullptr, *b2s = nullptr, *b3 = nullptr;
+    void *w2p = nullptr, *zp = nullptr;
+    int64_t bytes = 0;
+    // host bookkeeping
+    std::vector<uint8_t> span_written;
+    int64_t span_hi = 0;
+    int phase = PH_RESET;
+    bool w2_ready = false;
+    const float *W2 = nullptr, *b2 = nullptr;
+};
+
+namespace {
+
+ts3_status check_desc(const ts3_desc *d) {
+    if (!d) return fail(TS3_ERR_INVALID_ARG, "desc is NULL");
+    if (d->C <= 0 || d->H <= 0 || d->M <= 0 || d->dh <= 0)
+        return fail(TS3_ERR_INVALID_ARG, "C, H, M, dh must be positive (got %d, %d, %d, %d)", d->C, d->H,
+                    d->M, d->dh);
+    if ((int64_t)d->H * d->dh != d->C)
+        return fail(TS3_ERR_UNSUPPORTED, "H*dh (%d*%d) must equal C (%d)", d->H, d->dh, d->C);
+    if (d->io_dtype != TS3_FP32 && d->io_dtype != TS3_BF16)
+        return fail(TS3_ERR_INVALID_ARG, "io_dtype %d is not TS3_FP32 or TS3_BF16", d->io_dtype);
+    if (!(d->temperature > 0.f)) return fail(TS3_ERR_INVALID_ARG, "temperature must be > 0");
+    if (!(d->eps >= 0.f) || std::isinf(d->eps)) return fail(TS3_ERR_INVALID_ARG, "eps must be finite and >= 0");
+    if (d->group_span <= 0 || d->group_span % 32 != 0 || d->group_span > (1 << 30))
+        return fail(TS3_ERR_INVALID_ARG, "group_span must be a positive multiple of 32 (got %lld)",
+                    (long long)d->group_span);
+    if (d->max_points < 0) return fail(TS3_ERR_INVALID_ARG, "max_points must be >= 0");
+    if (d->H > 4096 || d->dh > 256) return fail(TS3_ERR_UNSUPPORTED, "H <= 4096 and dh <= 256 required");
+    Kernels k;
+    if (!find_kernels(d->io_dtype, d->C, d->M, &k))
+        return fail(TS3_ERR_UNSUPPORTED, "no kernel for C=%d, M=%d (supported: C in {64,128} with "
+                    "M in {16,32}, or C=128 with M=64)", d->C, d->M);
+    if ((5 * d->M * d->dh + d->M * d->M) * 4 > ATTN_LDS_MAX)
+        return fail(TS3_ERR_UNSUPPORTED, "token attention needs (5*M*dh + M*M) floats <= 160 KiB of LDS");
+    const int64_t nspan = (d->max_points + d->group_span - 1) / d->group_span;
+    if (nspan * (int64_t)d->H > (int64_t)INT32_MAX)
+        return fail(TS3_ERR_UNSUPPORTED, "too many spans: raise group_span");
+    return TS3_OK;
+}
+
+ts3_status check_weights_w2(const ts3_weights *w) {
+    if (!w) return fail(TS3_ERR_INVALID_ARG, "weights is NULL");
+    if (!w->W2) return fail(TS3_ERR_INVALID_ARG, "W2 is NULL");
+    return TS3_OK;
+}
+
+ts3_status prep_w2(ts3_state *st, const ts3_weights *w, hipStream_t stream) {
+    const ts3_desc &d = st->desc;
+    const float scale = (float)(1.4426950408889634 / (double)d.temperature);
+    const int64_t total = (int64_t)d.H * (d.M / 16) * (d.C / 32) * 512;
+    const int grid = (int)std::min<int64_t>((total + 255) / 256, 4096);
+    const int grid2 = std::max(grid, (d.H * d.M + 255) / 256);
+    if (d.io_dtype == TS3_BF16)
+        hipLaunchKernelGGL(k_prep_w2<bf16_t>, dim3(grid2), dim3(256), 0, stream, w->W2, w->b2, scale, d.C,
+                           d.H, d.M, (bf16_t *)st->w2p, st->b2s);
+    else
+        hipLaunchKernelGGL(k_prep_w2<float>, dim3(grid2), dim3(256), 0, stream, w->W2, w->b2, scale, d.C,
+                           d.H, d.M, (float *)st->w2p, st->b2s);
+    LAUNCH_CHECK("prep_w2");
+    st->W2 = w->W2;
+    st->b2 = w->b2;
+    st->w2_ready = true;
+    return TS3_OK;
+}
+
+ts3_status prep_z(ts3_state *st, hipStream_t stream) {
+    const ts3_desc &d = st->desc;
+    const int KM = d.M >= 32 ? d.M / 32 : 1;
+    const int64_t total = (int64_t)d.H * (d.C / 16) * KM * 512;
+    const int grid = (int)std::min<int64_t>((total + 255) / 256, 4096);
+    if (d.io_dtype == TS3_BF16)
+        hipLaunchKernelGGL(k_prep_z<bf16_t>, dim3(grid), dim3(256), 0, stream, st->Z, d.C, d.H, d.M,
+                           (bf16_t *)st->zp);
+    else
+        hipLaunchKernelGGL(k_prep_z<float>, dim3(grid), dim3(256), 0, stream, st->Z, d.C, d.H, d.M,
+                           (float *)st->zp);
+    LAUNCH_CHECK("prep_z");
+    return TS3_OK;
+}
+
+bool same_w2(const ts3_state *st, const ts3_weights *w) { return w->W2 == st->W2 && w->b2 == st->b2; }
+
+}  // namespace
+
+extern "C" {
+
+const char *ts3_status_string(ts3_status s) {
+    switch (s) {
+        case TS3_OK: return "ok";
+        case TS3_ERR_INVALID_ARG: return "invalid argument";
+        case TS3_ERR_BAD_STATE: return "call out of order";
+        case TS3_ERR_OUT_OF_MEMORY: return "out of device memory";
+        case TS3_ERR_HIP: return "HIP runtime error";
+        case TS3_ERR_UNSUPPORTED: return "unsupported shape";
+    }
+    return "unknown status";
+}
+
+const char *ts3_last_error(void) { return g_err.c_str(); }
+
+ts3_status ts3_state_free(ts3_state *st) {
+    if (!st) return TS3_OK;
+    hipError_t e = hipDeviceSynchronize();
+    void *bufs[] = {st->partials, st->runs, st->s_raw, st->dsum, st->s, st->s1,
+                    st->Z,        st->b2s,  st->b3,    st->w2p,  st->zp};
+    for (void *b : bufs)
+        if (b) (void)hipFree(b);
+    delete st;
+    if (e != hipSuccess) return fail(TS3_ERR_HIP, "hipDeviceSynchronize: %s", hipGetErrorString(e));
+    return TS3_OK;
+}
+
+ts3_status ts3_state_create(const ts3_desc *desc, ts3_state **out) {
+    if (!out) return fail(TS3_ERR_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    ts3_status s = check_desc(desc);
+    if (s != TS3_OK) return s;
+    ts3_state *st = new (std::nothrow) ts3_state();
+    if (!st) return fail(TS3_ERR_OUT_OF_MEMORY, "host allocation failed");
+    st->desc = *desc;
+    find_kernels(desc->io_dtype, desc->C, desc->M, &st->k);
+    const ts3_desc &d = st->desc;
+    st->esize = d.io_dtype == TS3_BF16 ? 2 : 4;
+    st->nspan_max = std::max<int64_t>(1, (d.max_points + d.group_span - 1) / d.group_span);
+    st->E = (int64_t)d.H * d.M * (d.C + 1);
+    st->nrun_max = (st->nspan_max + FOLD - 1) / FOLD;
+    const int64_t HM = (int64_t)d.H * d.M;
+    const int KM = d.M >= 32 ? d.M / 32 : 1;
+    struct Req {
+        void **p;
+        int64_t bytes;
+    } reqs[] = {
+        {(void **)&st->partials, st->nspan_max * st->E * 4},
+        {(void **)&st->runs, st->nrun_max * st->E * 4},
+        {(void **)&st->s_raw, HM * d.C * 4},
+        {(void **)&st->dsum, HM * 4},
+        {(void **)&st->s, HM * d.dh * 4},
+        {(void **)&st->s1, HM * d.dh * 4},
+        {(void **)&st->Z, HM * d.C * 4},
+        {(void **)&st->b2s, HM * 4},
+        {(void **)&st->b3, (int64_t)d.C * 4},
+        {&st->w2p, (int64_t)d.H * (d.M / 16) * (d.C / 32) * 512 * st->esize},
+        {&st->zp, (int64_t)d.H * (d.C / 16) * KM * 512 * st->esize},
+    };
+    for (auto &r : reqs) {
+        hipError_t e = hipMalloc(r.p, (size_t)r.bytes);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            ts3_state_free(st);
+            return fail(e == hipErrorOutOfMemory ? TS3_ERR_OUT_OF_MEMORY : TS3_ERR_HIP,
+                        "hipMalloc(%lld bytes): %s", (long long)r.bytes, hipGetErrorString(e));
+        }
+        st->bytes += r.bytes;
+    }
+    st->span_written.assign((size_t)st->nspan_max, 0);
+    *out = st;
+    return TS3_OK;
+}
+
+ts3_status ts3_state_bytes(const ts3_state *st, int64_t *bytes) {
+    if (!st || !bytes) return fail(TS3_ERR_INVALID_ARG, "NULL argument");
+    *bytes = st->bytes;
+    return TS3_OK;
+}
+
+ts3_status ts3_state_reset(ts3_state *st, void *stream) {
+    (void)stream;
+    if (!st) return fail(TS3_ERR_INVALID_ARG, "state is NULL");
+    std::fill(st->span_written.begin(), st->span_written.end(), 0);
+    st->span_hi = 0;
+    st->phase = PH_RESET;
+    st->w2_ready = false;
+    st->W2 = st->b2 = nullptr;
+    return TS3_OK;
+}
+
+ts3_status ts3_slice_accumulate(ts3_state *st, const ts3_weights *w, const void *x_tile, int64_t n_tile,
+                                int64_t point_offset, void *stream) {
+    if (!st) return fail(TS3_ERR_INVALID_ARG, "state is NULL");
+    ts3_status s = check_weights_w2(w);
+    if (s != TS3_OK) return s;
+    if (st->phase != PH_RESET && st->phase != PH_ACCUM)
+        return fail(TS3_ERR_BAD_STATE, "accumulate after finalize: call ts3_state_reset first");
+    if (n_tile < 0 || point_offset < 0) return fail(TS3_ERR_INVALID_ARG, "negative size or offset");
+    if (n_tile == 0) return TS3_OK;
+    if (!x_tile) return fail(TS3_ERR_INVALID_ARG, "x_tile is NULL");
+    if (((uintptr_t)x_tile & 15) != 0) return fail(TS3_ERR_INVALID_ARG, "x_tile must be 16-byte aligned");
+    const ts3_desc &d = st->desc;
+    const int64_t Q = d.group_span;
+    if (point_offset % Q != 0)
+        return fail(TS3_ERR_INVALID_ARG, "point_offset %lld is not a multiple of group_span %lld",
+                    (long long)point_offset, (long long)Q);
+    if (point_offset + n_tile > d.max_points)
+        return fail(TS3_ERR_INVALID_ARG, "tile end %lld exceeds max_points %lld",
+                    (long long)(point_offset + n_tile), (long long)d.max_points);
+    if (st->w2_ready && !same_w2(st, w))
+        return fail(TS3_ERR_INVALID_ARG, "W2/b2 differ from the ones recorded at the first accumulate");
+    const int64_t span0 = point_offset / Q;
+    const int64_t nspan = (n_tile + Q - 1) / Q;
+    const bool ragged = n_tile % Q != 0;
+    for (int64_t i = span0; i < span0 + nspan; ++i)
+        if (st->span_written[(size_t)i])
+            return fail(TS3_ERR_INVALID_ARG, "tile overlaps span %lld accumulated earlier", (long long)i);
+    // A ragged (short) last span must hold the mesh's last point: no written span may follow it.
+    if (ragged && span0 + nspan < st->span_hi)
+        return fail(TS3_ERR_INVALID_ARG, "a tile ending inside a span must be the mesh's last tile");
+    for (int64_t i = 0; i < span0; ++i)
+        if (st->span_written[(size_t)i] == 2)
+            return fail(TS3_ERR_INVALID_ARG, "a tile ending inside a span was accumulated before this one");
+    hipStream_t hs = (hipStream_t)stream;
+    if (!st->w2_ready) {
+        s = prep_w2(st, w, hs);
+        if (s != TS3_OK) return s;
+    }
+    st->k.pass1(x_tile, n_tile, span0, (int32_t)Q, (int32_t)nspan, d.H, st->w2p, st->b2s, st->partials, hs);
+    LAUNCH_CHECK("slice_accumulate");
+    for (int64_t i = span0; i < span0 + nspan; ++i) st->span_written[(size_t)i] = 1;
+    if (ragged) st->span_written[(size_t)(span0 + nspan - 1)] = 2;
+    st->span_hi = std::max(st->span_hi, span0 + nspan);
+    st->phase = PH_ACCUM;
+    return TS3_OK;
+}
+
+ts3_status ts3_slice_finalize(ts3_state *st, const ts3_weights *w, void *stream) {
+    if (!st) return fail(TS3_ERR_INVALID_ARG, "state is NULL");
+    if (!w || !w->W1) return fail(TS3_ERR_INVALID_ARG, "weights or W1 is NULL");
+    if (st->phase != PH_RESET && st->phase != PH_ACCUM)
+        return fail(TS3_ERR_BAD_STATE, "finalize needs a reset or accumulating state");
+    const ts3_desc &d = st->desc;
+    hipStream_t hs = (hipStream_t)stream;
+    const int64_t E = st->E;
+    const int64_t nspan = std::max<int64_t>(st->span_hi, 1);
+    // Spans below span_hi that no tile wrote contribute zero.
+    for (int64_t i = 0; i < nspan; ++i) {
+        if (st->span_written[(size_t)i]) continue;
+        int64_t j = i;
+        while (j < nspan && !st->span_written[(size_t)j]) ++j;
+        const int64_t cnt = (j - i) * E;
+        hipLaunchKernelGGL(k_zero, dim3((unsigned)std::min<int64_t>((cnt + 255) / 256, 65535)), dim3(256), 0,
+                           hs, st->partials + i * E, cnt);
+        LAUNCH_CHECK("zero spans");
+        i = j;
+    }
+    const int64_t nrun = (nspan + FOLD - 1) / FOLD;
+    const unsigned gx = (unsigned)((E + 255) / 256);
+    hipLaunchKernelGGL(k_fold_runs, dim3(gx, (unsigned)nrun), dim3(256), 0, hs, st->partials, E, nspan, st->runs);
+    LAUNCH_CHECK("fold_runs");
+    hipLaunchKernelGGL(k_fold_final, dim3(gx), dim3(256), 0, hs, st->runs, E, nrun, d.C, st->s_raw, st->dsum);
+    LAUNCH_CHECK("fold_final");
+    const size_t lds = (size_t)d.M * d.C * 4;
+    hipLaunchKernelGGL(k_finalize, dim3(d.H), dim3(256), lds, hs, st->s_raw, st->dsum, w->W1, w->b1, d.C, d.H,
+                       d.M, d.dh, d.eps, st->s);
+    LAUNCH_CHECK("finalize");
+    st->phase = PH_FINAL;
+    return TS3_OK;
+}
+
+ts3_status ts3_token_attention(ts3_state *st, const ts3_weights *w, void *stream) {
+    if (!st) return fail(TS3_ERR_INVALID_ARG, "state is NULL");
+    if (!w || !w->Wq || !w->Wk || !w->Wv || !w->W3)
+        return fail(TS3_ERR_INVALID_ARG, "weights, Wq, Wk, Wv or W3 is NULL");
+    if (st->phase != PH_FINAL) return fail(TS3_ERR_BAD_STATE, "token_attention needs a finalized state");
+    const ts3_desc &d = st->desc;
+    hipStream_t hs = (hipStream_t)stream;
+    const size_t lds = (size_t)(5 * d.M * d.dh + d.M * d.M) * 4;
+    if (lds > 64 * 1024)
+        HIP_TRY(hipFuncSetAttribute((const void *)k_attention, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                    ATTN_LDS_MAX));
+    hipLaunchKernelGGL(k_attention, dim3(d.H), dim3(256), lds, hs, st->s, w->Wq, w->Wk, w->Wv, w->W3, d.C, d.H,
+                       d.M, d.dh, st->s1, st->Z);
+    LAUNCH_CHECK("attention");
+    ts3_status s = prep_z(st, hs);
+    if (s != TS3_OK) return s;
+    if (w->b3)
+        HIP_TRY(hipMemcpyAsync(st->b3, w->b3, (size_t)d.C * 4, hipMemcpyDeviceToDevice, hs));
+    else
+        hipLaunchKernelGGL(k_zero, dim3(1), dim3(256), 0, hs, st->b3, (int64_t)d.C);
+    LAUNCH_CHECK("b3");
+    st->phase = PH_ATTEND;
+    return TS3_OK;
+}
+
+ts3_status ts3_deslice(const ts3_state *st, const ts3_weights *w, const void *x_chunk, int64_t n_chunk,
+                       void *out_chunk, void *stream) {
+    if (!st) return fail(TS3_ERR_INVALID_ARG, "state is NULL");
+    ts3_status s = check_weights_w2(w);
+    if (s != TS3_OK) return s;
+    if (st->phase != PH_ATTEND) return fail(TS3_ERR_BAD_STATE, "deslice needs the cached state (attention)");
+    if (!same_w2(st, w)) return fail(TS3_ERR_INVALID_ARG, "W2/b2 differ from the ones recorded for this state");
+    if (n_chunk < 0) return fail(TS3_ERR_INVALID_ARG, "negative n_chunk");
+    if (n_chunk == 0) return TS3_OK;
+    if (!x_chunk || !out_chunk) return fail(TS3_ERR_INVALID_ARG, "x_chunk or out_chunk is NULL");
+    if (((uintptr_t)x_chunk & 15) || ((uintptr_t)out_chunk & 15))
+        return fail(TS3_ERR_INVALID_ARG, "x_chunk and out_chunk must be 16-byte aligned");
+    const ts3_desc &d = st->desc;
+    if (n_chunk > ((int64_t)INT32_MAX) * 64) return fail(TS3_ERR_INVALID_ARG, "n_chunk too large for one launch");
+    st->k.pass2(x_chunk, n_chunk, d.H, st->w2p, st->b2s, st->zp, st->b3, out_chunk, (hipStream_t)stream);
+    LAUNCH_CHECK("deslice");
+    return TS3_OK;
+}
+
+ts3_status ts3_layer_forward(ts3_state *st, const ts3_weights *w, const void *x, int64_t N, int64_t tile,
+                             int64_t chunk, void *out, void *stream) {
+    if (!st) return fail(TS3_ERR_INVALID_ARG, "state is NULL");
+    if (N < 0 || tile <= 0 || chunk <= 0) return fail(TS3_ERR_INVALID_ARG, "N >= 0, tile > 0, chunk > 0 required");
+    if (tile % st->desc.group_span != 0)
+        return fail(TS3_ERR_INVALID_ARG, "tile %lld is not a multiple of group_span %lld", (long long)tile,
+                    (long long)st->desc.group_span);
+    if (N > 0 && (!x || !out)) return fail(TS3_ERR_INVALID_ARG, "x or out is NULL");
+    ts3_status s = ts3_state_reset(st, stream);
+    const char *xb = (const char *)x;
+    char *ob = (char *)out;
+    const int64_t row = (int64_t)st->desc.C * st->esize;
+    for (int64_t t0 = 0; s == TS3_OK && t0 < N; t0 += tile)
+        s = ts3_slice_accumulate(st, w, xb + t0 * row, std::min(tile, N - t0), t0, stream);
+    if (s == TS3_OK && N == 0 && (!w || !w->W2)) s = check_weights_w2(w);
+    if (s == TS3_OK && !st->w2_ready) s = prep_w2(st, w, (hipStream_t)stream);
+    if (s == TS3_OK) s = ts3_slice_finalize(st, w, stream);
+    if (s == TS3_OK) s = ts3_token_attention(st, w, stream);
+    for (int64_t c0 = 0; s == TS3_OK && c0 < N; c0 += chunk)
+        s = ts3_deslice(st, w, xb + c0 * row, std::min(chunk, N - c0), ob + c0 * row, stream);
+    return s;
+}
+
+ts3_status ts3_state_get(const ts3_state *st, int32_t which, float *host_dst, int64_t n, void *stream) {
+    if (!st || !host_dst) return fail(TS3_ERR_INVALID_ARG, "NULL argument");
+    const ts3_desc &d = st->desc;
+    const int64_t HM = (int64_t)d.H * d.M;
+    const float *src = nullptr;
+    int64_t size = 0;
+    int need = PH_FINAL;
+    switch (which) {
+        case TS3_S_RAW: src = st->s_raw; size = HM * d.C; break;
+        case TS3_D: src = st->dsum; size = HM; break;
+        case TS3_S: src = st->s; size = HM * d.dh; break;
+        case TS3_S1: src = st->s1; size = HM * d.dh; need = PH_ATTEND; break;
+        case TS3_ZP: src = st->Z; size = HM * d.C; need = PH_ATTEND; break;
+        default: return fail(TS3_ERR_INVALID_ARG, "unknown buffer %d", which);
+    }
+    if (n != size) return fail(TS3_ERR_INVALID_ARG, "buffer %d holds %lld floats, not %lld", which,
+                                (long long)size, (long long)n);
+    if (st->phase < need) return fail(TS3_ERR_BAD_STATE, "buffer %d is not computed yet", which);
+    hipStream_t hs = (hipStream_t)stream;
+    HIP_TRY(hipMemcpyAsync(host_dst, src, (size_t)size * 4, hipMemcpyDeviceToHost, hs));
+    HIP_TRY(hipStreamSynchronize(hs));
+    return TS3_OK;
+}
+
+ts3_status ts3_state_set(ts3_state *st, const ts3_weights *w, int32_t which, const float *host_src, int64_t n,
+                         const float *host_b3, void *stream) {
+    if (!st || !host_src) return fail(TS3_ERR_INVALID_ARG, "NULL argument");
+    ts3_status s = check_weights_w2(w);
+    if (s != TS3_OK) return s;
+    if (which != TS3_ZP) return fail(TS3_ERR_INVALID_ARG, "only TS3_ZP can be set");
+    const ts3_desc &d = st->desc;
+    const int64_t size = (int64_t)d.H * d.M * d.C;
+    if (n != size) return fail(TS3_ERR_INVALID_ARG, "Z holds %lld floats, not %lld", (long long)size, (long long)n);
+    hipStream_t hs = (hipStream_t)stream;
+    HIP_TRY(hipMemcpyAsync(st->Z, host_src, (size_t)size * 4, hipMemcpyHostToDevice, hs));
+    std::vector<float> b3(d.C, 0.f);
+    if (host_b3) std::memcpy(b3.data(), host_b3, (size_t)d.C * 4);
+    HIP_TRY(hipMemcpyAsync(st->b3, b3.data(), (size_t)d.C * 4, hipMemcpyHostToDevice, hs));
+    s = prep_z(st, hs);
+    if (s == TS3_OK) s = prep_w2(st, w, hs);
+    if (s != TS3_OK) return s;
+    HIP_TRY(hipStreamSynchronize(hs));
+    st->phase = PH_ATTEND;
+    return TS3_OK;
+}
+
+}  // extern "C"

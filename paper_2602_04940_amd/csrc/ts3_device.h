@@ -1,0 +1,130 @@
+// Device helpers for the gfx950 Physics-Attention kernels: matrix-core
+// fragment types, the 16x16 MFMA wrappers and cross-lane reductions.
+//
+// Fragment convention (every MFMA in this library is 16x16 with a K step of
+// 32): lane l of a wave64 owns row/column (l & 15) of an operand and "K slots"
+// (g, t) with g = l >> 4 in 0..3 and t in 0..7.  A and B operands pair slot
+// (g, t) with slot (g, t), so which reduction index a slot holds is a free
+// choice made per contraction, as long as both operands agree.  Output
+// fragment (4 floats): lane l holds D[4*g + r][l & 15], r = 0..3.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ts3 {
+
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+
+struct bf16_t {
+    uint16_t bits;
+};
+
+// An 8-slot operand fragment for one K32 step.
+template <typename T> struct Frag;
+
+template <> struct Frag<float> {
+    float v[8];
+    __device__ __forceinline__ void set(int t, float x) { v[t] = x; }
+};
+
+template <> struct Frag<bf16_t> {
+    bf16x8 v;
+    __device__ __forceinline__ void set(int t, float x) { v[t] = (__bf16)x; }
+};
+
+// acc += A * B over one K32 step.
+__device__ __forceinline__ void mma(f32x4 &acc, const Frag<bf16_t> &a, const Frag<bf16_t> &b) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v, b.v, acc, 0, 0, 0);
+}
+__device__ __forceinline__ void mma(f32x4 &acc, const Frag<float> &a, const Frag<float> &b) {
+#pragma unroll
+    for (int t = 0; t < 8; ++t) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.v[t], b.v[t], acc, 0, 0, 0);
+}
+
+// Load the 8 consecutive storage elements at p (16 B for bf16, 32 B for fp32).
+__device__ __forceinline__ void load8(Frag<bf16_t> &f, const bf16_t *p) {
+    f.v = *reinterpret_cast<const bf16x8 *>(p);
+}
+__device__ __forceinline__ void load8(Frag<float> &f, const float *p) {
+    const float4 a = reinterpret_cast<const float4 *>(p)[0];
+    const float4 b = reinterpret_cast<const float4 *>(p)[1];
+    f.v[0] = a.x; f.v[1] = a.y; f.v[2] = a.z; f.v[3] = a.w;
+    f.v[4] = b.x; f.v[5] = b.y; f.v[6] = b.z; f.v[7] = b.w;
+}
+__device__ __forceinline__ void zero8(Frag<bf16_t> &f) {
+    f.v = bf16x8{};
+}
+__device__ __forceinline__ void zero8(Frag<float> &f) {
+#pragma unroll
+    for (int t = 0; t < 8; ++t) f.v[t] = 0.f;
+}
+__device__ __forceinline__ void ones8(Frag<bf16_t> &f) {
+#pragma unroll
+    for (int t = 0; t < 8; ++t) f.v[t] = (__bf16)1.0f;
+}
+__device__ __forceinline__ void ones8(Frag<float> &f) {
+#pragma unroll
+    for (int t = 0; t < 8; ++t) f.v[t] = 1.f;
+}
+
+// Storage element <-> float.
+__device__ __forceinline__ float to_f32(float x) { return x; }
+__device__ __forceinline__ float to_f32(bf16_t x) { return __uint_as_float(uint32_t(x.bits) << 16); }
+__device__ __forceinline__ uint16_t raw16(bf16_t x) { return x.bits; }
+
+// Element t of a loaded fragment as stored bits/values (for LDS transposes).
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
+__device__ __forceinline__ uint16_t elem_bits(const Frag<bf16_t> &f, int t) {
+    // Read element t through the packed dwords (element 2k is the low half of dword k).
+    const u32x4 u = __builtin_bit_cast(u32x4, f.v);
+    return (uint16_t)((t & 1) ? (u[t >> 1] >> 16) : (u[t >> 1] & 0xffffu));
+}
+__device__ __forceinline__ float elem_f32(const Frag<float> &f, int t) { return f.v[t]; }
+
+// Cross-lane reductions among the 16 lanes of a DPP row (all lanes get the result).
+template <int CTRL> __device__ __forceinline__ float dpp(float v) {
+    return __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(v), CTRL, 0xf, 0xf, false));
+}
+__device__ __forceinline__ float row16_max(float v) {
+    v = fmaxf(v, dpp<0x128>(v));  // row_ror:8
+    v = fmaxf(v, dpp<0x124>(v));  // row_ror:4
+    v = fmaxf(v, dpp<0x4E>(v));   // quad_perm [2,3,0,1]
+    v = fmaxf(v, dpp<0xB1>(v));   // quad_perm [1,0,3,2]
+    return v;
+}
+__device__ __forceinline__ float row16_sum(float v) {
+    v += dpp<0x128>(v);
+    v += dpp<0x124>(v);
+    v += dpp<0x4E>(v);
+    v += dpp<0xB1>(v);
+    return v;
+}
+
+// Reductions across the four 16-lane rows (lanes l, l^16, l^32, l^48).
+__device__ __forceinline__ float xrow_max(float v) {
+    auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float xrow_sum(float v) {
+    auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
+
+// XCD-aware block index: consecutive logical indices land on the same XCD
+// (workgroups are dispatched round-robin over the 8 XCDs of an MI355X).
+__device__ __forceinline__ int xcd_remap(int i, int n) {
+    const int xcd = i & 7, k = i >> 3;
+    const int base = n >> 3, rem = n & 7;
+    return xcd < rem ? xcd * (base + 1) + k : rem * (base + 1) + (xcd - rem) * base + k;
+}
+
+}  // namespace ts3

@@ -1,0 +1,148 @@
+// Pass 2 of the Physics-Attention layer: full-mesh decoding against the cached
+// state (paper Eq. (5), Algorithm 1 deslice loop).  The slice weights are
+// recomputed from x and never stored:
+//     out[p] = sum_h sum_m softmax_m(L_h[p]) Z[h][m][:] + b3.
+//
+// Work decomposition: each wave decodes a block of 16*PT points over all
+// heads, so the sum over heads stays in its accumulator registers.
+// Per head:
+//   logits  L[m][p] = W2'[:, h*M+m] . x[p] + b2'  16x16x32 MFMA with A = W2'^T
+//           fragments, B = x^T (the wave's point rows, loaded once per block).
+//           Output lane (g, p) holds slices 4g+r of each 16-slice tile, so the
+//           softmax over m is an in-lane pass plus two cross-row swaps.
+//   deslice out[c][p] += Z[h]^T[c][m] . w[m][p]: A = prepared Z fragments
+//           whose K slots follow the logits' register order, B = w straight
+//           from registers.
+#pragma once
+#include "ts3_device.h"
+
+namespace ts3 {
+
+template <typename T, int C, int M> struct Pass2Cfg {
+    static constexpr int CT = C / 16;
+    static constexpr int MT = M / 16;
+    static constexpr int CK = C / 32;
+    static constexpr int KM = M >= 32 ? M / 32 : 1;  // K32 steps over slices (M=16 pads half a step)
+    static constexpr int PT = sizeof(T) == 2 ? 4 : 2;  // 16-point tiles per wave block
+    static constexpr int WAVES = 4;
+    static constexpr int POINTS_PER_WG = WAVES * 16 * PT;
+};
+
+// x   : [n][C] storage elements; out: [n][C]
+// w2p : prepared W2' fragments [H][MT][CK][64][8] (also the A = W2'^T layout)
+// b2s : scaled bias [H*M]
+// zp  : prepared Z fragments [H][CT][KM][64][8]
+// b3  : [C] float32
+template <typename T, int C, int M>
+__global__ __launch_bounds__(256, 1) void k_deslice(const T *__restrict__ x, int64_t n, int32_t H,
+                                                    const T *__restrict__ w2p,
+                                                    const float *__restrict__ b2s,
+                                                    const T *__restrict__ zp,
+                                                    const float *__restrict__ b3, T *__restrict__ out) {
+    using Cfg = Pass2Cfg<T, C, M>;
+    constexpr int CT = Cfg::CT, MT = Cfg::MT, CK = Cfg::CK, KM = Cfg::KM, PT = Cfg::PT;
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int li = lane & 15;
+    const int g = lane >> 4;
+    const int64_t p0 = ((int64_t)blockIdx.x * Cfg::WAVES + wave) * (16 * PT);
+    if (p0 >= n) return;
+
+    // B operand x^T: lane (g, li) holds x[p0 + 16*pt + li][32*kc + 8*g .. +8].
+    Frag<T> xb[PT][CK];
+#pragma unroll
+    for (int pt = 0; pt < PT; ++pt) {
+        const int64_t p = p0 + pt * 16 + li;
+#pragma unroll
+        for (int kc = 0; kc < CK; ++kc) {
+            if (p < n)
+                load8(xb[pt][kc], x + (size_t)p * C + kc * 32 + g * 8);
+            else
+                zero8(xb[pt][kc]);
+        }
+    }
+
+    f32x4 O[CT][PT];
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+        for (int pt = 0; pt < PT; ++pt) O[ct][pt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    for (int h = 0; h < H; ++h) {
+        f32x4 L[MT][PT];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            const float4 bb = *reinterpret_cast<const float4 *>(b2s + h * M + mt * 16 + g * 4);
+#pragma unroll
+            for (int pt = 0; pt < PT; ++pt) L[mt][pt] = f32x4{bb.x, bb.y, bb.z, bb.w};
+#pragma unroll
+            for (int kc = 0; kc < CK; ++kc) {
+                Frag<T> a;
+                load8(a, w2p + ((((size_t)h * MT + mt) * CK + kc) * 64 + lane) * 8);
+#pragma unroll
+                for (int pt = 0; pt < PT; ++pt) mma(L[mt][pt], a, xb[pt][kc]);
+            }
+        }
+
+        // Softmax over the head's M slices for point 16*pt + li.
+        Frag<T> wf[PT][KM];
+#pragma unroll
+        for (int pt = 0; pt < PT; ++pt) {
+            float mx = L[0][pt][0];
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) mx = fmaxf(mx, L[mt][pt][r]);
+            mx = xrow_max(mx);
+            float sum = 0.f;
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const float e = fast_exp2(L[mt][pt][r] - mx);
+                    L[mt][pt][r] = e;
+                    sum += e;
+                }
+            const float inv = fast_rcp(xrow_sum(sum));
+#pragma unroll
+            for (int km = 0; km < KM; ++km)
+#pragma unroll
+                for (int t = 0; t < 8; ++t) {
+                    const int mt = 2 * km + (t >> 2);
+                    wf[pt][km].set(t, mt < MT ? L[mt][pt][t & 3] * inv : 0.f);
+                }
+        }
+
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+            for (int km = 0; km < KM; ++km) {
+                Frag<T> a;
+                load8(a, zp + ((((size_t)h * CT + ct) * KM + km) * 64 + lane) * 8);
+#pragma unroll
+                for (int pt = 0; pt < PT; ++pt) mma(O[ct][pt], a, wf[pt][km]);
+            }
+    }
+
+    // Store: lane (g, li) holds out[p0 + 16*pt + li][16*ct + 4*g + r].
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct) {
+        const float4 bb = *reinterpret_cast<const float4 *>(b3 + ct * 16 + g * 4);
+#pragma unroll
+        for (int pt = 0; pt < PT; ++pt) {
+            const int64_t p = p0 + pt * 16 + li;
+            if (p >= n) continue;
+            const float v0 = O[ct][pt][0] + bb.x, v1 = O[ct][pt][1] + bb.y;
+            const float v2 = O[ct][pt][2] + bb.z, v3 = O[ct][pt][3] + bb.w;
+            T *dst = out + (size_t)p * C + ct * 16 + g * 4;
+            if constexpr (sizeof(T) == 2) {
+                typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
+                *reinterpret_cast<bf16x4 *>(dst) = bf16x4{(__bf16)v0, (__bf16)v1, (__bf16)v2, (__bf16)v3};
+            } else {
+                *reinterpret_cast<float4 *>(dst) = float4{v0, v1, v2, v3};
+            }
+        }
+    }
+}
+
+}  // namespace ts3

@@ -1,0 +1,298 @@
+"""GPU parity: the HIP path through the C ABI against the float64 oracle.
+
+Bars: float32 storage -> normwise max relative error <= 1e-4; bfloat16
+storage with float32 accumulation -> relative L2 <= 2e-2.  Tiled and untiled
+runs, tile order, and reruns must agree bitwise.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+from gpu_helpers import banner, normwise, rel_l2, to_device, to_host
+from ts3_synth import WORKLOADS, make_weights
+from ts3_synth.workloads import small_features
+
+pytestmark = pytest.mark.gpu
+
+FP32_TOL = 1e-4
+BF16_TOL = 2e-2
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _layer(C, H, M, dtype, tau=0.5, Q=1024, max_points=1 << 16, eps=0.0):
+    from paper_2602_04940_amd import PhysicsAttention
+    return PhysicsAttention(C, H, M, C // H, tau, dtype, group_span=Q, max_points=max_points, eps=eps)
+
+
+def _weights(W):
+    from paper_2602_04940_amd import LayerWeights
+    return LayerWeights(W)
+
+
+def _state(layer):
+    from paper_2602_04940_amd import _lib as L
+    return {"s_raw": layer.get(L.TS3_S_RAW), "d": layer.get(L.TS3_D), "s": layer.get(L.TS3_S),
+            "s1": layer.get(L.TS3_S1), "Z": layer.get(L.TS3_ZP)}
+
+
+def _run(x64, W, C, H, M, dtype, tau, tile, chunk, Q, eps=0.0):
+    torch = _torch()
+    x = to_device(x64, dtype)
+    lw = _weights(W)
+    with _layer(C, H, M, dtype, tau, Q, max(len(x64), 1), eps) as layer:
+        out = layer.forward(lw, x, tile=tile, chunk=chunk)
+        torch.cuda.synchronize()
+        return to_host(out), _state(layer), out
+
+
+# ------------------------------------------------------------ named workloads
+
+def test_fp32_ellipsoid_4k_layer_and_state():
+    wl = WORKLOADS["ellipsoid_4k_fp32"]
+    banner(f"{wl.name}: N={wl.N} C={wl.C} H={wl.H} M={wl.M} fp32")
+    x = small_features(wl, wl.N)
+    W = make_weights(wl.C, wl.H, wl.M, wl.dh, seed=0)
+    got, st, _ = _run(x, W, wl.C, wl.H, wl.M, "fp32", wl.tau, tile=wl.tile, chunk=wl.chunk, Q=1024)
+    ref_st = oracle.build_state(x, W, wl.H, wl.M, 1 / wl.tau)
+    for k in ("s_raw", "d", "s", "s1", "Z"):
+        assert normwise(st[k], ref_st[k]) <= FP32_TOL, k
+    ref = oracle.layer_forward_fast(x, W, wl.H, wl.M, 1 / wl.tau)
+    err = normwise(got, ref)
+    print(f"normwise max rel err {err:.3e}")
+    assert err <= FP32_TOL
+
+
+@pytest.fixture(scope="module")
+def ellipsoid_1m():
+    wl = WORKLOADS["ellipsoid_1m_bf16"]
+    banner(f"{wl.name}: generating inputs")
+    x = small_features(wl, wl.N)
+    W = make_weights(wl.C, wl.H, wl.M, wl.dh, seed=0)
+    banner(f"{wl.name}: oracle pass 1")
+    Z = oracle.build_state(x, W, wl.H, wl.M, 1 / wl.tau, tile=wl.tile)["Z"]
+    banner(f"{wl.name}: oracle pass 2")
+    ref = np.concatenate([oracle.deslice(x[c:c + wl.chunk], W["W2"], W["b2"], Z, W["b3"], wl.H, wl.M,
+                                         1 / wl.tau) for c in range(0, wl.N, wl.chunk)])
+    return wl, x, W, ref, Z
+
+
+def test_bf16_ellipsoid_1m_tiled_matches_oracle_and_untiled_bitwise(ellipsoid_1m):
+    torch = _torch()
+    wl, x, W, ref, Zref = ellipsoid_1m
+    banner(f"{wl.name}: N={wl.N} tile={wl.tile} Q={wl.group_span} bf16")
+    got, st, out_t = _run(x, W, wl.C, wl.H, wl.M, "bf16", wl.tau, wl.tile, wl.chunk, wl.group_span)
+    e_out, e_z = rel_l2(got, ref), rel_l2(st["Z"], Zref)
+    print(f"rel L2 out {e_out:.3e}  Z {e_z:.3e}")
+    assert e_out <= BF16_TOL and e_z <= BF16_TOL
+    one_tile = -(-wl.N // wl.group_span) * wl.group_span
+    got1, st1, out_1 = _run(x, W, wl.C, wl.H, wl.M, "bf16", wl.tau, one_tile, wl.N, wl.group_span)
+    assert np.array_equal(st1["Z"], st["Z"]) and np.array_equal(st1["s_raw"], st["s_raw"])
+    assert torch.equal(out_1, out_t)
+
+
+# ------------------------------------------------------------ shape sweep
+
+SHAPES = [(64, 4, 16), (64, 4, 32), (64, 1, 32), (128, 8, 16), (128, 8, 32), (128, 8, 64), (128, 2, 64)]
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("C,H,M", SHAPES)
+def test_shapes_ragged_tiles_random_biases(C, H, M, dtype):
+    N, Q, tile, chunk = 1000, 128, 384, 333
+    banner(f"shape C={C} H={H} M={M} {dtype} N={N} tile={tile} Q={Q}")
+    rng = np.random.default_rng(C * 1000 + H * 10 + M)
+    x = rng.standard_normal((N, C))
+    if dtype == "bf16":
+        from ts3_synth import round_bf16
+        x = round_bf16(x)
+    else:
+        x = x.astype(np.float32).astype(np.float64)
+    W = make_weights(C, H, M, C // H, seed=3, bias_seed=4)
+    got, st, _ = _run(x, W, C, H, M, dtype, 0.5, tile, chunk, Q)
+    ref = oracle.layer_forward_fast(x, W, H, M, 2.0)
+    ref_st = oracle.build_state(x, W, H, M, 2.0)
+    if dtype == "fp32":
+        assert normwise(got, ref) <= FP32_TOL
+        for k in ("s_raw", "d", "Z"):
+            assert normwise(st[k], ref_st[k]) <= FP32_TOL, k
+    else:
+        assert rel_l2(got, ref) <= BF16_TOL
+        for k in ("s_raw", "d", "Z"):
+            assert rel_l2(st[k], ref_st[k]) <= BF16_TOL, k
+
+
+# ------------------------------------------------------------ special cases
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_infinite_temperature_gives_mean_pool(dtype):
+    C, H, M, N = 64, 4, 32, 777
+    banner(f"1/tau=0 {dtype}")
+    rng = np.random.default_rng(1)
+    from ts3_synth import round_storage
+    x = round_storage(rng.standard_normal((N, C)), dtype)
+    W = make_weights(C, H, M, C // H, seed=5, bias_seed=6)
+    got, st, _ = _run(x, W, C, H, M, dtype, math.inf, 256, 500, 128)
+    ref = oracle.layer_forward_fast(x, W, H, M, 0.0)
+    tol = FP32_TOL if dtype == "fp32" else BF16_TOL
+    err = normwise(got, ref) if dtype == "fp32" else rel_l2(got, ref)
+    assert err <= tol
+    np.testing.assert_allclose(st["d"], N / M, rtol=1e-5 if dtype == "fp32" else 1e-2)
+
+
+def test_one_hot_slices_fp32():
+    C, H, M, N = 64, 4, 16, 1024
+    banner("one-hot slices fp32")
+    rng = np.random.default_rng(2)
+    x = rng.standard_normal((3 * N, C)).astype(np.float32).astype(np.float64)
+    W = make_weights(C, H, M, C // H, seed=7)
+    # keep points whose two largest logits differ by > 0.05 in every head (weights are one-hot)
+    lg = np.sort((x @ W["W2"].astype(np.float64)).reshape(-1, H, M), axis=2)
+    x = x[((lg[:, :, -1] - lg[:, :, -2]) > 0.05).all(axis=1)][:N]
+    assert len(x) == N
+    got, st, _ = _run(x, W, C, H, M, "fp32", 1.0 / 200.0, 512, 512, 256)
+    ref_st = oracle.build_state(x, W, H, M, 200.0)
+    assert normwise(st["s_raw"], ref_st["s_raw"]) <= FP32_TOL
+    assert normwise(st["d"], ref_st["d"]) <= FP32_TOL
+    ref = oracle.layer_forward_fast(x, W, H, M, 200.0)
+    assert normwise(got, ref) <= FP32_TOL
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_permuted_and_duplicated_points(dtype):
+    torch = _torch()
+    C, H, M, N = 128, 8, 32, 640
+    banner(f"permutation/duplication {dtype}")
+    rng = np.random.default_rng(3)
+    from ts3_synth import round_storage
+    x = round_storage(rng.standard_normal((N, C)), dtype)
+    W = make_weights(C, H, M, C // H, seed=8)
+    got, st, _ = _run(x, W, C, H, M, dtype, 0.5, 640, 640, 64)
+    perm = rng.permutation(N)
+    got_p, st_p, _ = _run(x[perm], W, C, H, M, dtype, 0.5, 640, 640, 64)
+    got_d, st_d, _ = _run(np.concatenate([x, x]), W, C, H, M, dtype, 0.5, 1280, 1280, 64)
+    f = normwise if dtype == "fp32" else rel_l2
+    tol = FP32_TOL if dtype == "fp32" else BF16_TOL
+    assert f(got_p, got[perm]) <= tol
+    assert f(st_p["Z"], st["Z"]) <= tol
+    assert f(st_d["Z"], st["Z"]) <= tol
+    assert f(got_d, np.concatenate([got, got])) <= tol
+
+
+def test_empty_mesh_and_empty_chunks():
+    torch = _torch()
+    C, H, M = 64, 4, 16
+    banner("empty mesh")
+    W = make_weights(C, H, M, C // H, seed=9, bias_seed=10)
+    lw = _weights(W)
+    with _layer(C, H, M, "fp32", Q=64, max_points=64) as layer:
+        x = torch.empty((0, C), device="cuda", dtype=torch.float32)
+        layer.forward(lw, x, tile=64, chunk=64)
+        st = _state(layer)
+        ref_st = oracle.build_state(np.zeros((0, C)), W, H, M, 2.0)
+        for k in ("s", "s1", "Z"):
+            assert normwise(st[k], ref_st[k]) <= FP32_TOL, k
+        y = layer.deslice(lw, x)
+        assert y.shape == (0, C)
+
+
+# ------------------------------------------------------------ determinism
+
+def test_rerun_and_reverse_tile_order_are_bitwise_identical():
+    torch = _torch()
+    C, H, M, N, Q = 128, 8, 64, 5000, 256
+    banner("determinism bf16 C=128 M=64")
+    rng = np.random.default_rng(4)
+    from ts3_synth import round_bf16
+    x64 = round_bf16(rng.standard_normal((N, C)))
+    W = make_weights(C, H, M, C // H, seed=11)
+    lw = _weights(W)
+    x = to_device(x64, "bf16")
+    with _layer(C, H, M, "bf16", Q=Q, max_points=N) as layer:
+        out_a = layer.forward(lw, x, tile=1024, chunk=999).clone()
+        Za = layer.get(4)
+        out_b = layer.forward(lw, x, tile=1024, chunk=4096).clone()
+        layer.reset()
+        starts = list(range(0, N, 512))[::-1]
+        for t0 in starts:
+            layer.accumulate(lw, x[t0:t0 + 512], t0)
+        layer.finalize(lw)
+        layer.attention(lw)
+        out_c = layer.deslice(lw, x)
+        Zc = layer.get(4)
+    torch.cuda.synchronize()
+    assert torch.equal(out_a, out_b) and torch.equal(out_a, out_c)
+    assert np.array_equal(Za, Zc)
+
+
+# ------------------------------------------------------------ pass 2 alone
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_deslice_with_injected_state(dtype):
+    torch = _torch()
+    C, H, M, N = 128, 8, 64, 3001
+    banner(f"deslice with injected Z {dtype}")
+    rng = np.random.default_rng(5)
+    from ts3_synth import round_storage
+    x64 = round_storage(rng.standard_normal((N, C)), dtype)
+    W = make_weights(C, H, M, C // H, seed=12, bias_seed=13)
+    Z = rng.standard_normal((H, M, C)) * 0.3
+    b3 = rng.standard_normal(C) * 0.1
+    lw = _weights(W)
+    with _layer(C, H, M, dtype, Q=128, max_points=N) as layer:
+        layer.set_state(lw, Z.astype(np.float32), b3.astype(np.float32))
+        out = layer.deslice(lw, to_device(x64, dtype))
+        torch.cuda.synchronize()
+    ref = oracle.deslice(x64, W["W2"], W["b2"], Z.astype(np.float32), b3.astype(np.float32), H, M, 2.0)
+    got = to_host(out)
+    if dtype == "fp32":
+        assert normwise(got, ref) <= FP32_TOL
+    else:
+        assert rel_l2(got, ref) <= BF16_TOL
+
+
+# ------------------------------------------------------------ error paths
+
+def test_call_order_and_argument_errors():
+    torch = _torch()
+    from paper_2602_04940_amd import _lib as L
+    C, H, M = 64, 4, 16
+    banner("error paths")
+    W = make_weights(C, H, M, C // H, seed=14)
+    lw = _weights(W)
+    lw2 = _weights(W)  # same values, different W2 pointer
+    x = torch.zeros((256, C), device="cuda", dtype=torch.float32)
+
+    def status(fn):
+        try:
+            fn()
+        except L.TS3Error as e:
+            return e.status
+        return L.TS3_OK
+
+    with _layer(C, H, M, "fp32", Q=64, max_points=512) as layer:
+        assert status(lambda: layer.deslice(lw, x)) == L.TS3_ERR_BAD_STATE
+        assert status(lambda: layer.attention(lw)) == L.TS3_ERR_BAD_STATE
+        assert status(lambda: layer.accumulate(lw, x[:64], 32)) == L.TS3_ERR_INVALID_ARG   # misaligned
+        assert status(lambda: layer.accumulate(lw, x, 320)) == L.TS3_ERR_INVALID_ARG       # past max_points
+        assert status(lambda: layer.accumulate(lw, x[:128], 0)) == L.TS3_OK
+        assert status(lambda: layer.accumulate(lw, x[:64], 64)) == L.TS3_ERR_INVALID_ARG   # overlap
+        assert status(lambda: layer.accumulate(lw2, x[:64], 128)) == L.TS3_ERR_INVALID_ARG  # other W2
+        assert status(lambda: layer.accumulate(lw, x[:40], 192)) == L.TS3_OK              # ragged last
+        assert status(lambda: layer.accumulate(lw, x[:64], 256)) == L.TS3_ERR_INVALID_ARG  # past the ragged end
+        assert status(lambda: layer.accumulate(lw, x[:64], 128)) == L.TS3_OK              # before it: fine
+        layer.finalize(lw)
+        assert status(lambda: layer.accumulate(lw, x[:64], 128)) == L.TS3_ERR_BAD_STATE
+        layer.attention(lw)
+        assert status(lambda: layer.deslice(lw2, x)) == L.TS3_ERR_INVALID_ARG
+        assert status(lambda: layer.deslice(lw, x)) == L.TS3_OK
+        torch.cuda.synchronize()
+    from paper_2602_04940_amd import PhysicsAttention
+    with pytest.raises(L.TS3Error) as e:
+        PhysicsAttention(C, H, M, C // H, 0.5, "fp32", group_span=32, max_points=10 ** 9)  # ~0.5 TB
+    assert e.value.status == L.TS3_ERR_OUT_OF_MEMORY
