@@ -1,0 +1,182 @@
+#!/usr/bin/env python3
+"""Benchmark: one Transolver-3 Physics-Attention layer forward on a 100M-point
+volume mesh (C=128, H=8 heads of M=64 slices, dh=16, tau=0.5, bf16 storage,
+1M-point tiles and decode chunks) on one MI355X.
+
+A step is the whole layer over the resident mesh: pass 1 over every tile,
+the ordered fold + Linear1 + token attention + Linear3, and pass 2 over every
+chunk.  x is generated on the device (seeded) before timing; the timed region
+covers exactly --steps steps between synchronised HIP events.  The line also
+carries the dominant kernel's roofline figures (HIP-event launch durations on
+the launch stream) and the float64 oracle's throughput on host cores over a
+bounded sample.  Prints one JSON line on stdout; progress goes to stderr.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "mesh points/s per Physics-Attention layer fwd @100M pts C=128; % roofline"
+PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 matrix peak (256 CU x 4096 flop/clk x 2.4 GHz)
+PEAK_HBM_GBS = 8000.0
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2602_04940_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel: str, launch_points: int):
+    """HBM bytes per launch from committed rocprofv3 --pmc summaries, if they were
+    taken on the current kernel sources; else None."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    k = t.get("kernels", {}).get(kernel)
+    if not k or t.get("source_hash") != kernel_source_hash() or k.get("points") != launch_points:
+        return None
+    return k.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(x_dev, W, wl, sample):
+    """The float64 oracle (as written) on the first `sample` points, host cores."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    import oracle
+    xs = x_dev[:sample].float().cpu().numpy().astype(np.float64)
+    it = 1.0 / wl.tau
+    t0 = time.perf_counter()
+    st = oracle.build_state(xs, W, wl.H, wl.M, it, tile=wl.tile)
+    for c in range(0, sample, wl.chunk):
+        oracle.deslice(xs[c:c + wl.chunk], W["W2"], W["b2"], st["Z"], W["b3"], wl.H, wl.M, it)
+    dt = time.perf_counter() - t0
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    return {"value": sample / dt, "unit": "points/s", "cores": threads, "kind": "oracle",
+            "sample": f"layer forward (pass 1, state, pass 2) in float64 numpy on the first {sample} "
+                      f"points of the mesh: {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--points", type=int, default=None, help="override N (quick runs)")
+    ap.add_argument("--cpu-sample", type=int, default=1_000_000)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU; --gpus {args.gpus} is not supported "
+              "(the layer shards by points with one all-gather of span partials; not built here)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2602_04940_amd import LayerWeights, PhysicsAttention
+    from ts3_synth import WORKLOADS, make_weights
+    from ts3_synth.device_gen import DeviceVolume
+
+    wl = WORKLOADS["volume_100m_bf16"]
+    N = args.points or wl.N
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    log(f"generating {N} volume points on the device (C={wl.C}, bf16)")
+    t0 = time.perf_counter()
+    x = torch.empty((N, wl.C), device=dev, dtype=torch.bfloat16)
+    DeviceVolume(wl.seed, wl.C, dev).fill(x, progress=lambda k: log(f"  chunk {k}/{-(-N // 1_000_000)}"))
+    out = torch.empty_like(x)
+    torch.cuda.synchronize()
+    log(f"inputs ready in {time.perf_counter() - t0:.1f} s")
+
+    W = make_weights(wl.C, wl.H, wl.M, wl.dh, seed=0)
+    lw = LayerWeights(W, dev)
+    layer = PhysicsAttention(wl.C, wl.H, wl.M, wl.dh, wl.tau, "bf16", group_span=wl.group_span, max_points=N)
+    free, total = torch.cuda.mem_get_info()
+    hbm_used_gb = (total - free) / 1e9
+
+    for i in range(args.warmup):
+        layer.forward(lw, x, tile=wl.tile, chunk=wl.chunk, out=out)
+    torch.cuda.synchronize()
+    log(f"warmup {args.warmup} done; timing {args.steps} steps")
+
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for i in range(args.steps):
+        layer.forward(lw, x, tile=wl.tile, chunk=wl.chunk, out=out)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / max(args.steps, 1)
+    log(f"{ms:.3f} ms/step")
+
+    # Per-pass launch durations on the launch stream (torch's current stream).
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    ntile = -(-N // wl.tile)
+    nchunk = -(-N // wl.chunk)
+    ev[0].record()
+    layer.reset()
+    for t in range(ntile):
+        layer.accumulate(lw, x[t * wl.tile:(t + 1) * wl.tile], t * wl.tile)
+    ev[1].record()
+    layer.finalize(lw)
+    layer.attention(lw)
+    ev[2].record()
+    for c in range(nchunk):
+        layer.deslice(lw, x[c * wl.chunk:(c + 1) * wl.chunk], out[c * wl.chunk:(c + 1) * wl.chunk])
+    ev[3].record()
+    torch.cuda.synchronize()
+    t_p1, t_mid, t_p2 = (ev[i].elapsed_time(ev[i + 1]) for i in range(3))
+    log(f"pass1 {t_p1:.3f} ms ({ntile} launches), state {t_mid:.3f} ms, pass2 {t_p2:.3f} ms ({nchunk} launches)")
+
+    flop_per_point = 4 * wl.C * wl.H * wl.M        # logits + contraction, per pass
+    if t_p1 >= t_p2:
+        kname, t_launch, nl = "k_slice_accumulate", t_p1 / ntile, ntile
+    else:
+        kname, t_launch, nl = "k_deslice", t_p2 / nchunk, nchunk
+    pts_launch = min(wl.tile, N)
+    achieved = flop_per_point * pts_launch / (t_launch * 1e-3) / 1e12
+    traffic = measured_traffic(kname, pts_launch)
+    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic, "kernel": kname,
+                "launch_ms": round(t_launch, 4), "launches": nl}
+
+    result = {
+        "metric": METRIC, "value": N / (ms * 1e-3), "unit": "points/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic: seeded volume mesh (box minus car-like body), Fourier features, device-generated",
+        "config": {"workload": wl.name, "N": N, "C": wl.C, "H": wl.H, "M": wl.M, "dh": wl.dh, "tau": wl.tau,
+                   "tile": wl.tile, "chunk": wl.chunk, "group_span": wl.group_span,
+                   "hbm_used_gb": round(hbm_used_gb, 2), "state_bytes": layer.bytes()},
+        "passes_ms": {"pass1": round(t_p1, 3), "state": round(t_mid, 3), "pass2": round(t_p2, 3)},
+        "roofline": roofline,
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        log(f"timing the float64 oracle on {args.cpu_sample} points (host cores)")
+        result["cpu_baseline"] = cpu_baseline(x, W, wl, min(args.cpu_sample, N))
+    layer.close()
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

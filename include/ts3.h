@@ -52,7 +52,8 @@ typedef enum { TS3_FP32 = 0, TS3_BF16 = 1 } ts3_dtype;
 /* Layer shape and numerics.
  *  C, H, M, dh : channels, heads, slices per head, head width; H*dh == C.
  *                Supported: (C, M) in {(64,16), (64,32), (128,16), (128,32),
- *                (128,64)}, dh == 16; otherwise TS3_ERR_UNSUPPORTED.
+ *                (128,64)} with (5*M*dh + M*M) * 4 bytes <= 160 KiB (the
+ *                token-attention working set); otherwise TS3_ERR_UNSUPPORTED.
  *  temperature : tau > 0 of the slice softmax; +inf gives uniform weights.
  *  eps         : added to d before the division in finalize (the paper uses 0).
  *                A slice with d + eps <= 0 has a zero mean state.
@@ -60,7 +61,7 @@ typedef enum { TS3_FP32 = 0, TS3_BF16 = 1 } ts3_dtype;
  *                the slice-weight and contraction products on bf16 matrix
  *                cores with float32 accumulation; TS3_FP32 uses float32
  *                matrix cores throughout.
- *  group_span  : Q, points per accumulation span (> 0, multiple of 32).  Pass 1
+ *  group_span  : Q, points per accumulation span (1 <= Q <= 2^30).  Pass 1
  *                reduces each span to one partial and sums spans in index
  *                order, so results do not depend on how the mesh is tiled.
  *  max_points  : largest point index + 1 the state will accumulate; sizes the

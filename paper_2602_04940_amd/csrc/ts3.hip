@@ -129,8 +129,8 @@ ts3_status check_desc(const ts3_desc *d) {
         return fail(TS3_ERR_INVALID_ARG, "io_dtype %d is not TS3_FP32 or TS3_BF16", d->io_dtype);
     if (!(d->temperature > 0.f)) return fail(TS3_ERR_INVALID_ARG, "temperature must be > 0");
     if (!(d->eps >= 0.f) || std::isinf(d->eps)) return fail(TS3_ERR_INVALID_ARG, "eps must be finite and >= 0");
-    if (d->group_span <= 0 || d->group_span % 32 != 0 || d->group_span > (1 << 30))
-        return fail(TS3_ERR_INVALID_ARG, "group_span must be a positive multiple of 32 (got %lld)",
+    if (d->group_span <= 0 || d->group_span > (1 << 30))
+        return fail(TS3_ERR_INVALID_ARG, "group_span must be in [1, 2^30] (got %lld)",
                     (long long)d->group_span);
     if (d->max_points < 0) return fail(TS3_ERR_INVALID_ARG, "max_points must be >= 0");
     if (d->H > 4096 || d->dh > 256) return fail(TS3_ERR_UNSUPPORTED, "H <= 4096 and dh <= 256 required");

@@ -51,7 +51,7 @@ def _desc(**kw):
     (dict(temperature=0.0), L.TS3_ERR_INVALID_ARG),
     (dict(temperature=float("nan")), L.TS3_ERR_INVALID_ARG),
     (dict(eps=-1.0), L.TS3_ERR_INVALID_ARG),
-    (dict(group_span=100), L.TS3_ERR_INVALID_ARG),
+    (dict(group_span=0), L.TS3_ERR_INVALID_ARG),
     (dict(max_points=-1), L.TS3_ERR_INVALID_ARG),
 ])
 def test_bad_descriptor_is_rejected_before_any_device_call(kw, status):
