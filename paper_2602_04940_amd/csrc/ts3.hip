@@ -48,6 +48,7 @@ ts3_status fail(ts3_status s, const char *fmt, ...) {
     } while (0)
 
 constexpr int ATTN_LDS_MAX = 160 * 1024;
+constexpr size_t PASS2_LDS_MAX = 160 * 1024;
 
 enum Phase { PH_RESET = 0, PH_ACCUM = 1, PH_FINAL = 2, PH_ATTEND = 3 };
 
@@ -66,13 +67,37 @@ void launch_pass1(const void *x, int64_t n, int64_t span0, int32_t Q, int32_t ns
                        (const T *)x, n, span0, Q, nspan, H, (const T *)w2p, b2s, partials);
 }
 
+int device_cu_count() {
+    static int cus = 0;
+    if (!cus) {
+        int dev = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+            cus = 256;
+    }
+    return cus;
+}
+
 template <typename T, int C, int M>
 void launch_pass2(const void *x, int64_t n, int32_t H, const void *w2p, const float *b2s,
                   const void *zp, const float *b3, void *out, hipStream_t st) {
     using Cfg = Pass2Cfg<T, C, M>;
-    const int64_t grid = (n + Cfg::POINTS_PER_WG - 1) / Cfg::POINTS_PER_WG;
-    hipLaunchKernelGGL((k_deslice<T, C, M>), dim3((unsigned)grid), dim3(256), 0, st, (const T *)x, n, H,
-                       (const T *)w2p, b2s, (const T *)zp, b3, (T *)out);
+    const int64_t nblk = (n + Cfg::POINTS_PER_WG - 1) / Cfg::POINTS_PER_WG;
+    const size_t lds = (size_t)H * M * C * sizeof(T) + (size_t)H * M * sizeof(float);
+    if (lds <= PASS2_LDS_MAX) {
+        static bool attr = false;
+        if (!attr) {
+            (void)hipFuncSetAttribute((const void *)k_deslice_lds<T, C, M>,
+                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)PASS2_LDS_MAX);
+            attr = true;
+        }
+        const int64_t grid = std::min<int64_t>(nblk, device_cu_count());
+        hipLaunchKernelGGL((k_deslice_lds<T, C, M>), dim3((unsigned)grid), dim3(256), lds, st, (const T *)x, n,
+                           H, (const T *)w2p, b2s, (const T *)zp, b3, (T *)out);
+    } else {
+        hipLaunchKernelGGL((k_deslice<T, C, M>), dim3((unsigned)nblk), dim3(256), 0, st, (const T *)x, n, H,
+                           (const T *)w2p, b2s, (const T *)zp, b3, (T *)out);
+    }
 }
 
 template <typename T, int C, int M> Kernels make_kernels() {

@@ -146,3 +146,163 @@ __global__ __launch_bounds__(256, 1) void k_deslice(const T *__restrict__ x, int
 }
 
 }  // namespace ts3
+
+namespace ts3 {
+
+// Pass 2 with the prepared W2' fragments of every head resident in LDS
+// (H*M*C storage elements; 128 KB for C=128, H*M=512 in bf16).  Persistent
+// workgroups stride over 4*16*PT-point blocks; Z fragments (16 KB per head)
+// stream through the L1 cache shared by the workgroup's four waves.  Each wave
+// issues head h-1's deslice MFMAs next to head h's softmax so the matrix cores
+// and the vector ALUs have independent instructions to overlap.
+template <typename T, int C, int M>
+__global__ __launch_bounds__(256, 1) void k_deslice_lds(const T *__restrict__ x, int64_t n, int32_t H,
+                                                        const T *__restrict__ w2p,
+                                                        const float *__restrict__ b2s,
+                                                        const T *__restrict__ zp,
+                                                        const float *__restrict__ b3, T *__restrict__ out) {
+    using Cfg = Pass2Cfg<T, C, M>;
+    constexpr int CT = Cfg::CT, MT = Cfg::MT, CK = Cfg::CK, KM = Cfg::KM, PT = Cfg::PT;
+    extern __shared__ __attribute__((aligned(16))) unsigned char lds_raw[];
+    T *w2l = reinterpret_cast<T *>(lds_raw);
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int li = lane & 15;
+    const int g = lane >> 4;
+
+    const int64_t w2_elems = (int64_t)H * MT * CK * 64 * 8;
+    float *b2l = reinterpret_cast<float *>(w2l + w2_elems);
+    {   // stage every head's W2' fragments and the scaled bias once
+        const int64_t total16 = w2_elems * (int64_t)sizeof(T) / 16;
+        const uint4 *src = reinterpret_cast<const uint4 *>(w2p);
+        uint4 *dst = reinterpret_cast<uint4 *>(w2l);
+        for (int64_t i = threadIdx.x; i < total16; i += 256) dst[i] = src[i];
+        for (int i = threadIdx.x; i < H * M; i += 256) b2l[i] = b2s[i];
+    }
+    __syncthreads();
+
+    const int64_t nblk = (n + Cfg::POINTS_PER_WG - 1) / Cfg::POINTS_PER_WG;
+    for (int64_t blk = blockIdx.x; blk < nblk; blk += gridDim.x) {
+        const int64_t p0 = (blk * Cfg::WAVES + wave) * (16 * PT);
+        if (p0 >= n) continue;
+
+        Frag<T> xb[PT][CK];
+#pragma unroll
+        for (int pt = 0; pt < PT; ++pt) {
+            const int64_t p = p0 + pt * 16 + li;
+#pragma unroll
+            for (int kc = 0; kc < CK; ++kc) {
+                if (p < n)
+                    load8(xb[pt][kc], x + (size_t)p * C + kc * 32 + g * 8);
+                else
+                    zero8(xb[pt][kc]);
+            }
+        }
+
+        f32x4 O[CT][PT];
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+            for (int pt = 0; pt < PT; ++pt) O[ct][pt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+        auto logits = [&](int h, f32x4 (&L)[MT][PT]) {
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+                const float4 bb = *reinterpret_cast<const float4 *>(b2l + h * M + mt * 16 + g * 4);
+#pragma unroll
+                for (int pt = 0; pt < PT; ++pt) L[mt][pt] = f32x4{bb.x, bb.y, bb.z, bb.w};
+#pragma unroll
+                for (int kc = 0; kc < CK; ++kc) {
+                    Frag<T> a;
+                    load8(a, w2l + ((((size_t)h * MT + mt) * CK + kc) * 64 + lane) * 8);
+#pragma unroll
+                    for (int pt = 0; pt < PT; ++pt) mma(L[mt][pt], a, xb[pt][kc]);
+                }
+            }
+        };
+
+        // Z fragments of one head, fetched a head ahead of their use.
+        Frag<T> zf[CT][KM];
+        auto fetch_z = [&](int h) {
+#pragma unroll
+            for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+                for (int km = 0; km < KM; ++km)
+                    load8(zf[ct][km], zp + ((((size_t)h * CT + ct) * KM + km) * 64 + lane) * 8);
+        };
+        // out += Z_h^T . w_h with Z_h in zf and w_h in wf.
+        auto deslice_head = [&](const Frag<T> (&wf)[PT][KM]) {
+#pragma unroll
+            for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+                for (int km = 0; km < KM; ++km)
+#pragma unroll
+                    for (int pt = 0; pt < PT; ++pt) mma(O[ct][pt], zf[ct][km], wf[pt][km]);
+        };
+
+        // Head h's softmax (VALU) runs while head h-1's deslice MFMAs drain.
+        Frag<T> wfa[PT][KM], wfb[PT][KM];
+        for (int h = 0; h < H; h += 2) {
+#pragma unroll
+            for (int half = 0; half < 2; ++half) {
+                const int hh = h + half;
+                if (hh >= H) break;
+                Frag<T>(&wcur)[PT][KM] = half == 0 ? wfa : wfb;
+                Frag<T>(&wprev)[PT][KM] = half == 0 ? wfb : wfa;
+                if (hh > 0) fetch_z(hh - 1);
+                f32x4 L[MT][PT];
+                logits(hh, L);
+                if (hh > 0) deslice_head(wprev);
+#pragma unroll
+                for (int pt = 0; pt < PT; ++pt) {
+                    float mx = L[0][pt][0];
+#pragma unroll
+                    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) mx = fmaxf(mx, L[mt][pt][r]);
+                    mx = xrow_max(mx);
+                    float sum = 0.f;
+#pragma unroll
+                    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            const float e = fast_exp2(L[mt][pt][r] - mx);
+                            L[mt][pt][r] = e;
+                            sum += e;
+                        }
+                    const float inv = fast_rcp(xrow_sum(sum));
+#pragma unroll
+                    for (int km = 0; km < KM; ++km)
+#pragma unroll
+                        for (int t = 0; t < 8; ++t) {
+                            const int mt = 2 * km + (t >> 2);
+                            wcur[pt][km].set(t, mt < MT ? L[mt][pt][t & 3] * inv : 0.f);
+                        }
+                }
+            }
+        }
+        fetch_z(H - 1);
+        deslice_head(((H - 1) & 1) ? wfb : wfa);
+
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) {
+            const float4 bb = *reinterpret_cast<const float4 *>(b3 + ct * 16 + g * 4);
+#pragma unroll
+            for (int pt = 0; pt < PT; ++pt) {
+                const int64_t p = p0 + pt * 16 + li;
+                if (p >= n) continue;
+                const float v0 = O[ct][pt][0] + bb.x, v1 = O[ct][pt][1] + bb.y;
+                const float v2 = O[ct][pt][2] + bb.z, v3 = O[ct][pt][3] + bb.w;
+                T *dst = out + (size_t)p * C + ct * 16 + g * 4;
+                if constexpr (sizeof(T) == 2) {
+                    typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
+                    *reinterpret_cast<bf16x4 *>(dst) = bf16x4{(__bf16)v0, (__bf16)v1, (__bf16)v2, (__bf16)v3};
+                } else {
+                    *reinterpret_cast<float4 *>(dst) = float4{v0, v1, v2, v3};
+                }
+            }
+        }
+    }
+}
+
+}  // namespace ts3
