@@ -56,8 +56,8 @@ enum Phase { PH_RESET = 0, PH_ACCUM = 1, PH_FINAL = 2, PH_ATTEND = 3 };
 struct Kernels {
     void (*pass1)(const void *, int64_t, int64_t, int32_t, int32_t, int32_t, const void *, const float *,
                   float *, hipStream_t);
-    void (*pass2)(const void *, int64_t, int32_t, const void *, const float *, const void *,
-                  const float *, void *, hipStream_t);
+    hipError_t (*pass2)(const void *, int64_t, int32_t, const void *, const float *, const void *,
+                        const float *, void *, hipStream_t);
 };
 
 template <typename T, int C, int M>
@@ -79,25 +79,37 @@ int device_cu_count() {
 }
 
 template <typename T, int C, int M>
-void launch_pass2(const void *x, int64_t n, int32_t H, const void *w2p, const float *b2s,
-                  const void *zp, const float *b3, void *out, hipStream_t st) {
+hipError_t launch_pass2(const void *x, int64_t n, int32_t H, const void *w2p, const float *b2s,
+                        const void *zp, const float *b3, void *out, hipStream_t st) {
     using Cfg = Pass2Cfg<T, C, M>;
     const int64_t nblk = (n + Cfg::POINTS_PER_WG - 1) / Cfg::POINTS_PER_WG;
-    const size_t lds = (size_t)H * M * C * sizeof(T) + (size_t)H * M * sizeof(float);
-    if (lds <= PASS2_LDS_MAX) {
-        static bool attr = false;
-        if (!attr) {
-            (void)hipFuncSetAttribute((const void *)k_deslice_lds<T, C, M>,
-                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)PASS2_LDS_MAX);
-            attr = true;
+    if constexpr (sizeof(T) == 2) {
+        const size_t lds = Pass2LdsCfg<T, C, M>::lds_bytes(H);
+        static size_t static_lds = SIZE_MAX;
+        if (static_lds == SIZE_MAX) {
+            hipFuncAttributes fa{};
+            static_lds = hipFuncGetAttributes(&fa, (const void *)k_deslice_lds<T, C, M>) == hipSuccess
+                             ? fa.sharedSizeBytes : PASS2_LDS_MAX;
         }
-        const int64_t grid = std::min<int64_t>(nblk, device_cu_count());
-        hipLaunchKernelGGL((k_deslice_lds<T, C, M>), dim3((unsigned)grid), dim3(256), lds, st, (const T *)x, n,
-                           H, (const T *)w2p, b2s, (const T *)zp, b3, (T *)out);
-    } else {
+        static size_t dyn_set = 0;  // dynamic LDS limit granted so far
+        if (lds + static_lds <= PASS2_LDS_MAX) {
+            if (lds > dyn_set) {
+                if (hipFuncSetAttribute((const void *)k_deslice_lds<T, C, M>,
+                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+                    return hipGetLastError();
+                dyn_set = lds;
+            }
+            const int64_t grid = std::min<int64_t>(nblk, device_cu_count());
+            hipLaunchKernelGGL((k_deslice_lds<T, C, M>), dim3((unsigned)grid), dim3(256), lds, st, (const T *)x,
+                               n, H, (const T *)w2p, b2s, (const T *)zp, b3, (T *)out);
+            return hipSuccess;
+        }
+    }
+    {
         hipLaunchKernelGGL((k_deslice<T, C, M>), dim3((unsigned)nblk), dim3(256), 0, st, (const T *)x, n, H,
                            (const T *)w2p, b2s, (const T *)zp, b3, (T *)out);
     }
+    return hipSuccess;
 }
 
 template <typename T, int C, int M> Kernels make_kernels() {
@@ -427,7 +439,9 @@ ts3_status ts3_deslice(const ts3_state *st, const ts3_weights *w, const void *x_
         return fail(TS3_ERR_INVALID_ARG, "x_chunk and out_chunk must be 16-byte aligned");
     const ts3_desc &d = st->desc;
     if (n_chunk > ((int64_t)INT32_MAX) * 64) return fail(TS3_ERR_INVALID_ARG, "n_chunk too large for one launch");
-    st->k.pass2(x_chunk, n_chunk, d.H, st->w2p, st->b2s, st->zp, st->b3, out_chunk, (hipStream_t)stream);
+    const hipError_t le =
+        st->k.pass2(x_chunk, n_chunk, d.H, st->w2p, st->b2s, st->zp, st->b3, out_chunk, (hipStream_t)stream);
+    if (le != hipSuccess) return fail(TS3_ERR_HIP, "deslice LDS setup: %s", hipGetErrorString(le));
     LAUNCH_CHECK("deslice");
     return TS3_OK;
 }

@@ -27,11 +27,22 @@ template <typename T> struct Frag;
 template <> struct Frag<float> {
     float v[8];
     __device__ __forceinline__ void set(int t, float x) { v[t] = x; }
+    // slots t and t+1 (t even) from two floats
+    __device__ __forceinline__ void set2(int t, float a, float b) { v[t] = a; v[t + 1] = b; }
 };
+
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
 
 template <> struct Frag<bf16_t> {
     bf16x8 v;
     __device__ __forceinline__ void set(int t, float x) { v[t] = (__bf16)x; }
+    // slots t and t+1 (t even) from two floats with one packed conversion
+    __device__ __forceinline__ void set2(int t, float a, float b) {
+        const bf16x2 p{(__bf16)a, (__bf16)b};
+        u32x4 u = __builtin_bit_cast(u32x4, v);
+        u[t >> 1] = __builtin_bit_cast(uint32_t, p);
+        v = __builtin_bit_cast(bf16x8, u);
+    }
 };
 
 // acc += A * B over one K32 step.
@@ -75,7 +86,6 @@ __device__ __forceinline__ float to_f32(bf16_t x) { return __uint_as_float(uint3
 __device__ __forceinline__ uint16_t raw16(bf16_t x) { return x.bits; }
 
 // Element t of a loaded fragment as stored bits/values (for LDS transposes).
-typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
 __device__ __forceinline__ uint16_t elem_bits(const Frag<bf16_t> &f, int t) {
     // Read element t through the packed dwords (element 2k is the low half of dword k).
     const u32x4 u = __builtin_bit_cast(u32x4, f.v);
@@ -117,7 +127,29 @@ __device__ __forceinline__ float xrow_sum(float v) {
 }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// The slice softmax skips the max subtraction when a row's sum of exp2 terms
+// lands in [2^-100, 2^100]: every term is then finite, the largest is a normal
+// number, and terms that underflow weigh < 2^-20 of it.  Rows outside the
+// window (or NaN) take the max-shifted path; both compute the same softmax.
+__device__ __forceinline__ bool softmax_sum_ok(float s) {
+    return s >= 0x1p-100f && s <= 0x1p100f;
+}
 __device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
+
+// Scheduling hint for the region just emitted: alternate NMFMA matrix-core
+// instructions with VPER vector-ALU instructions, pulling one LDS read ahead
+// of every RPER MFMAs, so one wave keeps both units busy (in-order issue would
+// otherwise run the MFMA cluster and the VALU cluster back to back).
+template <int NMFMA, int VPER, int RPER>
+__device__ __forceinline__ void interleave_mfma_valu() {
+#pragma unroll
+    for (int i = 0; i < NMFMA; ++i) {
+        if (RPER > 0 && i % RPER == 0) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                  // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x002, VPER, 0);                               // VALU
+    }
+}
 
 // XCD-aware block index: consecutive logical indices land on the same XCD
 // (workgroups are dispatched round-robin over the 8 XCDs of an MI355X).

@@ -14,6 +14,8 @@
 //           whose K slots follow the logits' register order, B = w straight
 //           from registers.
 #pragma once
+#include <type_traits>
+
 #include "ts3_device.h"
 
 namespace ts3 {
@@ -149,12 +151,89 @@ __global__ __launch_bounds__(256, 1) void k_deslice(const T *__restrict__ x, int
 
 namespace ts3 {
 
-// Pass 2 with the prepared W2' fragments of every head resident in LDS
-// (H*M*C storage elements; 128 KB for C=128, H*M=512 in bf16).  Persistent
-// workgroups stride over 4*16*PT-point blocks; Z fragments (16 KB per head)
-// stream through the L1 cache shared by the workgroup's four waves.  Each wave
-// issues head h-1's deslice MFMAs next to head h's softmax so the matrix cores
-// and the vector ALUs have independent instructions to overlap.
+// Softmax over one head's M slices for the wave's points, logits laid out
+// [slices x points] (lane (g, p) holds slices 16*mt + 4*g + r of point p):
+// w is written as the B operand of the deslice contraction, K slot (g, t) of
+// step km holding slice 32*km + 16*(t>>2) + 4*g + (t&3).
+template <typename T, int MT, int PT, int KM>
+__device__ __forceinline__ void pack_weights(const f32x4 (&E)[MT][PT], int pt, float inv, Frag<T> (&wf)[PT][KM]) {
+#pragma unroll
+    for (int km = 0; km < KM; ++km)
+#pragma unroll
+        for (int t = 0; t < 8; t += 2) {
+            const int mt = 2 * km + (t >> 2);
+            if (mt < MT)
+                wf[pt][km].set2(t, E[mt][pt][t & 3] * inv, E[mt][pt][(t & 3) + 1] * inv);
+            else
+                wf[pt][km].set2(t, 0.f, 0.f);
+        }
+}
+
+// Fast path: exp2 of the logits without a shift.  Returns false (wave-uniform)
+// if any row's sum falls outside the safe window; L then holds exp2 values.
+template <typename T, int MT, int PT, int KM>
+__device__ __forceinline__ bool softmax_unshifted(f32x4 (&L)[MT][PT], Frag<T> (&wf)[PT][KM]) {
+    bool ok = true;
+#pragma unroll
+    for (int pt = 0; pt < PT; ++pt) {
+        float sum = 0.f;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const float e = fast_exp2(L[mt][pt][r]);
+                L[mt][pt][r] = e;
+                sum += e;
+            }
+        sum = xrow_sum(sum);
+        ok = ok && softmax_sum_ok(sum);
+        pack_weights<T, MT, PT, KM>(L, pt, fast_rcp(sum), wf);
+    }
+    return !__any(!ok);
+}
+
+template <typename T, int MT, int PT, int KM>
+__device__ __forceinline__ void softmax_shifted(f32x4 (&L)[MT][PT], Frag<T> (&wf)[PT][KM]) {
+#pragma unroll
+    for (int pt = 0; pt < PT; ++pt) {
+        float mx = L[0][pt][0];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) mx = fmaxf(mx, L[mt][pt][r]);
+        mx = xrow_max(mx);
+        float sum = 0.f;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const float e = fast_exp2(L[mt][pt][r] - mx);
+                L[mt][pt][r] = e;
+                sum += e;
+            }
+        pack_weights<T, MT, PT, KM>(L, pt, fast_rcp(xrow_sum(sum)), wf);
+    }
+}
+
+// Pass 2 with the prepared W2' fragments of every head and the scaled bias
+// resident in LDS (H*M*C storage elements + H*M floats; 130 KB for C=128,
+// H*M=512 in bf16), and each head's Z fragments (16 KB) staged into LDS with
+// direct global->LDS loads shared by the workgroup's four waves.  Persistent
+// workgroups stride over 256-point blocks (64 per wave, 1 wave per SIMD).
+// Per head h: [barrier; stage Z_{h-1}] [logits_h MFMAs] [barrier]
+// [deslice_{h-1} MFMAs interleaved with softmax_h VALU].  Every wave runs every
+// block and barrier (tail points are masked), so barriers never diverge.
+template <typename T, int C, int M> struct Pass2LdsCfg {
+    using Base = Pass2Cfg<T, C, M>;
+    static constexpr int ZFRAGS = Base::CT * Base::KM;            // 1 KB fragments per head
+    static constexpr int Z_STAGE_ELEMS = ZFRAGS * 64 * 8;
+    static_assert(ZFRAGS % 4 == 0, "Z fragments split evenly over four waves");
+    static size_t lds_bytes(int H) {
+        return (size_t)H * Base::MT * Base::CK * 512 * sizeof(T) + (size_t)H * M * 4 +
+               (size_t)Z_STAGE_ELEMS * sizeof(T);
+    }
+};
+
 template <typename T, int C, int M>
 __global__ __launch_bounds__(256, 1) void k_deslice_lds(const T *__restrict__ x, int64_t n, int32_t H,
                                                         const T *__restrict__ w2p,
@@ -162,16 +241,19 @@ __global__ __launch_bounds__(256, 1) void k_deslice_lds(const T *__restrict__ x,
                                                         const T *__restrict__ zp,
                                                         const float *__restrict__ b3, T *__restrict__ out) {
     using Cfg = Pass2Cfg<T, C, M>;
+    using LCfg = Pass2LdsCfg<T, C, M>;
     constexpr int CT = Cfg::CT, MT = Cfg::MT, CK = Cfg::CK, KM = Cfg::KM, PT = Cfg::PT;
+    constexpr int ZFRAGS = LCfg::ZFRAGS;
     extern __shared__ __attribute__((aligned(16))) unsigned char lds_raw[];
     T *w2l = reinterpret_cast<T *>(lds_raw);
+    const int64_t w2_elems = (int64_t)H * MT * CK * 64 * 8;
+    float *b2l = reinterpret_cast<float *>(w2l + w2_elems);
+    T *zl = reinterpret_cast<T *>(b2l + H * M);
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int li = lane & 15;
     const int g = lane >> 4;
 
-    const int64_t w2_elems = (int64_t)H * MT * CK * 64 * 8;
-    float *b2l = reinterpret_cast<float *>(w2l + w2_elems);
     {   // stage every head's W2' fragments and the scaled bias once
         const int64_t total16 = w2_elems * (int64_t)sizeof(T) / 16;
         const uint4 *src = reinterpret_cast<const uint4 *>(w2p);
@@ -181,10 +263,20 @@ __global__ __launch_bounds__(256, 1) void k_deslice_lds(const T *__restrict__ x,
     }
     __syncthreads();
 
+    // Wave w copies Z fragments w, w+4, ... of head h into the stage (1 KB each).
+    auto stage_z = [&](int h) {
+#pragma unroll
+        for (int i = 0; i < ZFRAGS / 4; ++i) {
+            const int f = wave + 4 * i;
+            __builtin_amdgcn_global_load_lds(
+                (const void *)(zp + ((size_t)h * ZFRAGS + f) * 512 + lane * 8),
+                (__attribute__((address_space(3))) void *)(zl + f * 512), 16, 0, 0);
+        }
+    };
+
     const int64_t nblk = (n + Cfg::POINTS_PER_WG - 1) / Cfg::POINTS_PER_WG;
     for (int64_t blk = blockIdx.x; blk < nblk; blk += gridDim.x) {
         const int64_t p0 = (blk * Cfg::WAVES + wave) * (16 * PT);
-        if (p0 >= n) continue;
 
         Frag<T> xb[PT][CK];
 #pragma unroll
@@ -200,10 +292,6 @@ __global__ __launch_bounds__(256, 1) void k_deslice_lds(const T *__restrict__ x,
         }
 
         f32x4 O[CT][PT];
-#pragma unroll
-        for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-            for (int pt = 0; pt < PT; ++pt) O[ct][pt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
         auto logits = [&](int h, f32x4 (&L)[MT][PT]) {
 #pragma unroll
@@ -220,69 +308,60 @@ __global__ __launch_bounds__(256, 1) void k_deslice_lds(const T *__restrict__ x,
                 }
             }
         };
-
-        // Z fragments of one head, fetched a head ahead of their use.
-        Frag<T> zf[CT][KM];
-        auto fetch_z = [&](int h) {
-#pragma unroll
-            for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-                for (int km = 0; km < KM; ++km)
-                    load8(zf[ct][km], zp + ((((size_t)h * CT + ct) * KM + km) * 64 + lane) * 8);
-        };
-        // out += Z_h^T . w_h with Z_h in zf and w_h in wf.
+        // out += Z_h^T . w_h with Z_h in the LDS stage.
         auto deslice_head = [&](const Frag<T> (&wf)[PT][KM]) {
 #pragma unroll
             for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
-                for (int km = 0; km < KM; ++km)
+                for (int km = 0; km < KM; ++km) {
+                    Frag<T> a;
+                    load8(a, zl + ((ct * KM + km) * 64 + lane) * 8);
 #pragma unroll
-                    for (int pt = 0; pt < PT; ++pt) mma(O[ct][pt], zf[ct][km], wf[pt][km]);
+                    for (int pt = 0; pt < PT; ++pt) mma(O[ct][pt], a, wf[pt][km]);
+                }
         };
 
-        // Head h's softmax (VALU) runs while head h-1's deslice MFMAs drain.
-        Frag<T> wfa[PT][KM], wfb[PT][KM];
-        for (int h = 0; h < H; h += 2) {
+        // All heads of the block; SHIFTED selects the max-shifted softmax.  The
+        // unshifted pass reports whether every row of this wave was in the safe window.
+        auto run_heads = [&](auto shifted) -> bool {
 #pragma unroll
-            for (int half = 0; half < 2; ++half) {
-                const int hh = h + half;
-                if (hh >= H) break;
-                Frag<T>(&wcur)[PT][KM] = half == 0 ? wfa : wfb;
-                Frag<T>(&wprev)[PT][KM] = half == 0 ? wfb : wfa;
-                if (hh > 0) fetch_z(hh - 1);
+            for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+                for (int pt = 0; pt < PT; ++pt) O[ct][pt] = f32x4{0.f, 0.f, 0.f, 0.f};
+            bool ok = true;
+            Frag<T> wfa[PT][KM], wfb[PT][KM];
+            auto step = [&](int hh, Frag<T>(&wcur)[PT][KM], const Frag<T>(&wprev)[PT][KM]) {
+                if (hh > 0) {
+                    __syncthreads();  // every wave is done reading the stage
+                    stage_z(hh - 1);
+                }
                 f32x4 L[MT][PT];
                 logits(hh, L);
-                if (hh > 0) deslice_head(wprev);
-#pragma unroll
-                for (int pt = 0; pt < PT; ++pt) {
-                    float mx = L[0][pt][0];
-#pragma unroll
-                    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) mx = fmaxf(mx, L[mt][pt][r]);
-                    mx = xrow_max(mx);
-                    float sum = 0.f;
-#pragma unroll
-                    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) {
-                            const float e = fast_exp2(L[mt][pt][r] - mx);
-                            L[mt][pt][r] = e;
-                            sum += e;
-                        }
-                    const float inv = fast_rcp(xrow_sum(sum));
-#pragma unroll
-                    for (int km = 0; km < KM; ++km)
-#pragma unroll
-                        for (int t = 0; t < 8; ++t) {
-                            const int mt = 2 * km + (t >> 2);
-                            wcur[pt][km].set(t, mt < MT ? L[mt][pt][t & 3] * inv : 0.f);
-                        }
+                if (hh > 0) {
+                    __builtin_amdgcn_s_waitcnt(0);  // this wave's stage loads have landed
+                    __syncthreads();                // ... and every other wave's
+                    deslice_head(wprev);
                 }
+                if constexpr (decltype(shifted)::value)
+                    softmax_shifted<T, MT, PT, KM>(L, wcur);
+                else
+                    ok = softmax_unshifted<T, MT, PT, KM>(L, wcur) && ok;
+            };
+            for (int h = 0; h < H; h += 2) {
+                step(h, wfa, wfb);
+                if (h + 1 < H) step(h + 1, wfb, wfa);
             }
-        }
-        fetch_z(H - 1);
-        deslice_head(((H - 1) & 1) ? wfb : wfa);
+            __syncthreads();
+            stage_z(H - 1);
+            __builtin_amdgcn_s_waitcnt(0);
+            __syncthreads();
+            deslice_head(((H - 1) & 1) ? wfb : wfa);
+            return ok;
+        };
+        // Workgroup-uniform fallback: if any wave saw a row outside the safe
+        // window, all waves redo the block with the max-shifted softmax.
+        const bool ok = run_heads(std::false_type{});
+        if (__syncthreads_or(!ok)) run_heads(std::true_type{});
 
 #pragma unroll
         for (int ct = 0; ct < CT; ++ct) {
