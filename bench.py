@@ -53,6 +53,71 @@ def measured_traffic(kernel: str, launch_points: int):
     return k.get("hbm_bytes_per_launch")
 
 
+CAL_BYTES = 1 << 30  # calibration copy: 1 GiB read, 1 GiB written
+
+
+def pmc_driver(points: int):
+    """Short workload for rocprofv3 --pmc: two layer forwards over `points`
+    points (1M-point launches), then one device-to-device copy of CAL_BYTES whose
+    counter readings calibrate FETCH_SIZE / WRITE_SIZE."""
+    import torch
+
+    from paper_2602_04940_amd import LayerWeights, PhysicsAttention
+    from ts3_synth import WORKLOADS, make_weights
+    from ts3_synth.device_gen import DeviceVolume
+    wl = WORKLOADS["volume_100m_bf16"]
+    x = torch.empty((points, wl.C), device="cuda", dtype=torch.bfloat16)
+    DeviceVolume(wl.seed, wl.C).fill(x)
+    out = torch.empty_like(x)
+    lw = LayerWeights(make_weights(wl.C, wl.H, wl.M, wl.dh, seed=0))
+    with PhysicsAttention(wl.C, wl.H, wl.M, wl.dh, wl.tau, "bf16", group_span=wl.group_span,
+                          max_points=points) as layer:
+        for _ in range(2):
+            layer.forward(lw, x, tile=wl.tile, chunk=wl.chunk, out=out)
+        torch.cuda.synchronize()
+    src = torch.empty(CAL_BYTES, device="cuda", dtype=torch.uint8).fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    log("pmc driver done")
+
+
+def summarize_traffic(fetch_dir: str, write_dir: str, command: str):
+    """profiles/traffic.json from two rocprofv3 --pmc runs of --pmc-driver."""
+    import csv
+    import glob
+
+    def rows(d):
+        f = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+        if not f:
+            raise SystemExit(f"no counter_collection.csv under {d}")
+        return list(csv.DictReader(open(f[0])))
+
+    out = {"source_hash": kernel_source_hash(), "command": command, "kernels": {}}
+    per = {}
+    for name, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        rs = [r for r in rows(d) if r["Counter_Name"] == name]
+        cal = [r for r in rs if "copyBuffer" in r["Kernel_Name"]][-1]
+        factor = CAL_BYTES / (float(cal["Counter_Value"]) * 1024.0)
+        out.setdefault("calibration", {})[name] = {"copy_bytes": CAL_BYTES, "counter_kib": float(cal["Counter_Value"]),
+                                                  "bytes_per_counted_byte": factor}
+        for kname in ("k_slice_accumulate", "k_deslice_lds"):
+            vals = [float(r["Counter_Value"]) for r in rs if kname + "<" in r["Kernel_Name"]]
+            per.setdefault(kname, {})[name] = (sum(vals) / len(vals), len(vals), factor)
+    for kname, d in per.items():
+        f_kib, n, f_fac = d["FETCH_SIZE"]
+        w_kib, _, w_fac = d["WRITE_SIZE"]
+        out["kernels"]["k_deslice" if kname == "k_deslice_lds" else kname] = {
+            "points": 1_000_000, "dispatches": n, "fetch_kib": f_kib, "write_kib": w_kib,
+            "hbm_bytes_per_launch": f_kib * 1024 * f_fac + w_kib * 1024 * w_fac}
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    os.makedirs(os.path.dirname(path), exist_ok=True)
+    with open(path, "w") as fh:
+        json.dump(out, fh, indent=1)
+    print(json.dumps(out, indent=1))
+
+
 def cpu_baseline(x_dev, W, wl, sample):
     """The float64 oracle (as written) on the first `sample` points, host cores."""
     import numpy as np
@@ -80,7 +145,17 @@ def main():
     ap.add_argument("--points", type=int, default=None, help="override N (quick runs)")
     ap.add_argument("--cpu-sample", type=int, default=1_000_000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--pmc-driver", action="store_true", help="short workload for rocprofv3 --pmc runs")
+    ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="write profiles/traffic.json from two --pmc runs of --pmc-driver")
+    ap.add_argument("--command", default="", help="command line recorded with --summarize-traffic")
     args = ap.parse_args()
+    if args.summarize_traffic:
+        summarize_traffic(*args.summarize_traffic, args.command)
+        return
+    if args.pmc_driver:
+        pmc_driver(args.points or 4_000_000)
+        return
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU; --gpus {args.gpus} is not supported "
               "(the layer shards by points with one all-gather of span partials; not built here)",

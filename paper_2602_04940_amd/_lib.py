@@ -55,12 +55,14 @@ class TS3Error(RuntimeError):
 
 
 def lib() -> ct.CDLL:
+    """The loaded library; TS3_LIB may name another build of it (default: in-tree)."""
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB):
-            raise RuntimeError(f"{LIB} is missing: build it with __graft_entry__.build() "
+        path = os.environ.get("TS3_LIB", LIB)
+        if not os.path.exists(path):
+            raise RuntimeError(f"{path} is missing: build it with __graft_entry__.build() "
                                "(the layer has no fallback path)")
-        L = ct.CDLL(LIB)
+        L = ct.CDLL(path)
         for name, (res, args) in SIGNATURES.items():
             fn = getattr(L, name)
             fn.restype, fn.argtypes = res, args

@@ -124,24 +124,26 @@ __global__ __launch_bounds__(256, 1) void k_slice_accumulate(
     unsigned char *xl = lds + wave * Cfg::WAVE_BYTES;   // [32 points][XROW bytes]
     unsigned char *wl = xl + 32 * XROW;                   // [32 points][WROW bytes]
 
-    for (int blk = wave; blk < nblk; blk += Cfg::WAVES) {
+    // x rows of a block as the logits B operand: lane (g, li) holds
+    // x[p0 + 16*pt + li][32*kc + 8*g .. +8] (zero past the span's end).
+    auto load_x = [&](int blk, Frag<T> (&xb)[2][CK]) {
         const int64_t p0 = p_begin + ((int64_t)blk << 5);
-        const int valid = (int)(p_end - p0 < 32 ? p_end - p0 : 32);
-
-        // x rows as the logits B operand: lane (g, li) holds
-        // x[p0 + 16*pt + li][32*kc + 8*g .. +8]; also stored to the LDS tile.
-        Frag<T> xb[2][CK];
 #pragma unroll
         for (int pt = 0; pt < 2; ++pt) {
-            const int pr = pt * 16 + li;
+            const int64_t pr = p0 + pt * 16 + li;
 #pragma unroll
             for (int kc = 0; kc < CK; ++kc) {
-                if (pr < valid)
-                    load8(xb[pt][kc], x + (size_t)(p0 + pr) * C + kc * 32 + g * 8);
+                if (blk < nblk && pr < p_end)
+                    load8(xb[pt][kc], x + (size_t)pr * C + kc * 32 + g * 8);
                 else
                     zero8(xb[pt][kc]);
             }
         }
+    };
+
+    auto process = [&](int blk, Frag<T> (&xb)[2][CK]) {
+        const int64_t p0 = p_begin + ((int64_t)blk << 5);
+        const int valid = (int)(p_end - p0 < 32 ? p_end - p0 : 32);
         asm volatile("" ::: "memory");
 #pragma unroll
         for (int pt = 0; pt < 2; ++pt)
@@ -248,6 +250,18 @@ __global__ __launch_bounds__(256, 1) void k_slice_accumulate(
             }
         }
         asm volatile("" ::: "memory");
+    };
+
+    // Block b+4's rows load into registers while block b computes.
+    Frag<T> xa[2][CK], xn[2][CK];
+    load_x(wave, xn);
+    for (int blk = wave; blk < nblk; blk += Cfg::WAVES) {
+#pragma unroll
+        for (int pt = 0; pt < 2; ++pt)
+#pragma unroll
+            for (int kc = 0; kc < CK; ++kc) xa[pt][kc] = xn[pt][kc];
+        load_x(blk + Cfg::WAVES, xn);
+        process(blk, xa);
     }
     (void)KM;
 

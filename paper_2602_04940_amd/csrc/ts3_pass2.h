@@ -220,9 +220,9 @@ __device__ __forceinline__ void softmax_shifted(f32x4 (&L)[MT][PT], Frag<T> (&wf
 // H*M=512 in bf16), and each head's Z fragments (16 KB) staged into LDS with
 // direct global->LDS loads shared by the workgroup's four waves.  Persistent
 // workgroups stride over 256-point blocks (64 per wave, 1 wave per SIMD).
-// Per head h: [barrier; stage Z_{h-1}] [logits_h MFMAs] [barrier]
-// [deslice_{h-1} MFMAs interleaved with softmax_h VALU].  Every wave runs every
-// block and barrier (tail points are masked), so barriers never diverge.
+// Per head h: [barrier; stage Z_h] [logits_h] [softmax_h] [barrier]
+// [deslice_h].  Every wave runs every block and barrier (tail points are
+// masked), so barriers never diverge.
 template <typename T, int C, int M> struct Pass2LdsCfg {
     using Base = Pass2Cfg<T, C, M>;
     static constexpr int ZFRAGS = Base::CT * Base::KM;            // 1 KB fragments per head
@@ -275,21 +275,33 @@ __global__ __launch_bounds__(256, 1) void k_deslice_lds(const T *__restrict__ x,
     };
 
     const int64_t nblk = (n + Cfg::POINTS_PER_WG - 1) / Cfg::POINTS_PER_WG;
-    for (int64_t blk = blockIdx.x; blk < nblk; blk += gridDim.x) {
-        const int64_t p0 = (blk * Cfg::WAVES + wave) * (16 * PT);
 
-        Frag<T> xb[PT][CK];
+    // B operand x^T of one block: lane (g, li) holds x[p0 + 16*pt + li][32*kc + 8*g .. +8].
+    auto load_x = [&](int64_t blk, Frag<T> (&xb)[PT][CK]) {
+        const int64_t p0 = (blk * Cfg::WAVES + wave) * (16 * PT);
 #pragma unroll
         for (int pt = 0; pt < PT; ++pt) {
             const int64_t p = p0 + pt * 16 + li;
 #pragma unroll
             for (int kc = 0; kc < CK; ++kc) {
-                if (p < n)
+                if (blk < nblk && p < n)
                     load8(xb[pt][kc], x + (size_t)p * C + kc * 32 + g * 8);
                 else
                     zero8(xb[pt][kc]);
             }
         }
+    };
+
+    // x of the next block is loaded during the current block's last head, so
+    // its latency (and the whole device's burst of block loads) overlaps compute.
+    Frag<T> xb[PT][CK], xnext[PT][CK];
+    load_x(blockIdx.x, xnext);
+    for (int64_t blk = blockIdx.x; blk < nblk; blk += gridDim.x) {
+        const int64_t p0 = (blk * Cfg::WAVES + wave) * (16 * PT);
+#pragma unroll
+        for (int pt = 0; pt < PT; ++pt)
+#pragma unroll
+            for (int kc = 0; kc < CK; ++kc) xb[pt][kc] = xnext[pt][kc];
 
         f32x4 O[CT][PT];
 
@@ -321,47 +333,42 @@ __global__ __launch_bounds__(256, 1) void k_deslice_lds(const T *__restrict__ x,
                 }
         };
 
-        // All heads of the block; SHIFTED selects the max-shifted softmax.  The
-        // unshifted pass reports whether every row of this wave was in the safe window.
-        auto run_heads = [&](auto shifted) -> bool {
+        // All heads of the block.  Per head: [barrier; stage Z_h] [logits_h]
+        // [softmax_h] [wait; barrier] [deslice_h].  SHIFTED selects the
+        // max-shifted softmax; the unshifted pass reports whether every row of
+        // this wave was in the safe window.  PREFETCH loads the next block's x
+        // once the last head's logits no longer need this block's.
+        auto run_heads = [&](auto shifted, bool prefetch) -> bool {
 #pragma unroll
             for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
                 for (int pt = 0; pt < PT; ++pt) O[ct][pt] = f32x4{0.f, 0.f, 0.f, 0.f};
             bool ok = true;
-            Frag<T> wfa[PT][KM], wfb[PT][KM];
-            auto step = [&](int hh, Frag<T>(&wcur)[PT][KM], const Frag<T>(&wprev)[PT][KM]) {
-                if (hh > 0) {
-                    __syncthreads();  // every wave is done reading the stage
-                    stage_z(hh - 1);
-                }
+            for (int hh = 0; hh < H; ++hh) {
+                __syncthreads();  // every wave is done reading the stage
+                stage_z(hh);
                 f32x4 L[MT][PT];
                 logits(hh, L);
-                if (hh > 0) {
-                    __builtin_amdgcn_s_waitcnt(0);  // this wave's stage loads have landed
-                    __syncthreads();                // ... and every other wave's
-                    deslice_head(wprev);
-                }
+                if (prefetch && hh == H - 1) load_x(blk + gridDim.x, xnext);
+                Frag<T> wf[PT][KM];
                 if constexpr (decltype(shifted)::value)
-                    softmax_shifted<T, MT, PT, KM>(L, wcur);
+                    softmax_shifted<T, MT, PT, KM>(L, wf);
                 else
-                    ok = softmax_unshifted<T, MT, PT, KM>(L, wcur) && ok;
-            };
-            for (int h = 0; h < H; h += 2) {
-                step(h, wfa, wfb);
-                if (h + 1 < H) step(h + 1, wfb, wfa);
+                    ok = softmax_unshifted<T, MT, PT, KM>(L, wf) && ok;
+                __builtin_amdgcn_s_waitcnt(0);  // this wave's stage loads have landed
+                __syncthreads();                // ... and every other wave's
+                deslice_head(wf);
             }
-            __syncthreads();
-            stage_z(H - 1);
-            __builtin_amdgcn_s_waitcnt(0);
-            __syncthreads();
-            deslice_head(((H - 1) & 1) ? wfb : wfa);
             return ok;
         };
         // Workgroup-uniform fallback: if any wave saw a row outside the safe
         // window, all waves redo the block with the max-shifted softmax.
-        const bool ok = run_heads(std::false_type{});
-        if (__syncthreads_or(!ok)) run_heads(std::true_type{});
+        const bool ok = run_heads(std::false_type{}, true);
+        if (__syncthreads_or(!ok)) {
+            load_x(blk, xb);
+            run_heads(std::true_type{}, false);
+            load_x(blk + gridDim.x, xnext);
+        }
 
 #pragma unroll
         for (int ct = 0; ct < CT; ++ct) {
