@@ -151,6 +151,30 @@ __device__ __forceinline__ void interleave_mfma_valu() {
     }
 }
 
+// Direct global->LDS copy of 16 bytes per lane: lane l's bytes land at LDS
+// byte lds_base + 16*l (lds_base wave-uniform).  Issued as inline assembly so
+// that the compiler's wait-count pass does not see an LDS write in flight and
+// hold every later LDS access until it lands; callers track completion
+// themselves with wait_vmcnt.  M0 carries the LDS base; the kernels that use
+// this have no other M0 user (gfx950 LDS instructions do not read M0).
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16(const void *src, uint32_t lds_base) {
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds_base) : "memory", "m0");
+}
+#pragma clang diagnostic pop
+__device__ __forceinline__ uint32_t lds_addr(const void *p) {
+    return __builtin_amdgcn_readfirstlane(
+        (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p);
+}
+
+// Wait until at most N vector-memory operations of this wave are outstanding
+// (other counters untouched).
+template <int N> __device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
 // XCD-aware block index: consecutive logical indices land on the same XCD
 // (workgroups are dispatched round-robin over the 8 XCDs of an MI355X).
 __device__ __forceinline__ int xcd_remap(int i, int n) {
