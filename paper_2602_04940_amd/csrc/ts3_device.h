@@ -151,6 +151,23 @@ __device__ __forceinline__ void interleave_mfma_valu() {
     }
 }
 
+// Scheduling hint for a region holding a chain of NMFMA matrix-core
+// instructions fed by LDS reads, next to an independent vector-ALU chain: the
+// first PRE reads go up front, then each MFMA is followed by VPER vector-ALU
+// instructions, and RN further reads are pulled in after every RPER MFMAs
+// (starting after MFMA R0); NW LDS writes close the region.
+template <int PRE, int NMFMA, int VPER, int R0, int RPER, int RN, int NW>
+__device__ __forceinline__ void interleave_chain() {
+    __builtin_amdgcn_sched_group_barrier(0x100, PRE, 0);
+#pragma unroll
+    for (int i = 0; i < NMFMA; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, VPER, 0);
+        if (i >= R0 && (i - R0) % RPER == 0) __builtin_amdgcn_sched_group_barrier(0x100, RN, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x200, NW, 0);
+}
+
 // Direct global->LDS copy of 16 bytes per lane: lane l's bytes land at LDS
 // byte lds_base + 16*l (lds_base wave-uniform).  Issued as inline assembly so
 // that the compiler's wait-count pass does not see an LDS write in flight and
@@ -161,6 +178,19 @@ __device__ __forceinline__ void interleave_mfma_valu() {
 #pragma clang diagnostic ignored "-Winline-asm"
 __device__ __forceinline__ void dma16(const void *src, uint32_t lds_base) {
     asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds_base) : "memory", "m0");
+}
+// The same copy with a wave-uniform global base and a per-lane 32-bit offset.
+template <int IMM> __device__ __forceinline__ void dma16s(uint32_t voff, const void *sbase, uint32_t lds_base) {
+    static_assert(IMM >= 0 && IMM < 4096, "global offset field");
+    const uint64_t b = (uint64_t)(uintptr_t)sbase;  // pin the base to scalar registers
+    // readfirstlane yields a signed int: widen through uint32_t so the low
+    // half is not sign-extended into the high one.
+    const uint64_t ub = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(b >> 32)) << 32) |
+                        (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)b);
+    sbase = (const void *)(uintptr_t)ub;
+    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1 offset:%3" ::"v"(voff), "s"(sbase),
+                 "s"(lds_base), "n"(IMM)
+                 : "memory", "m0");
 }
 #pragma clang diagnostic pop
 __device__ __forceinline__ uint32_t lds_addr(const void *p) {

@@ -11,23 +11,25 @@
 // Spans are folded in index order later, so the result is a fixed function of
 // (x, Q) whatever the tiling.
 //
-// Per 32-point block and wave:
-//   x rows   arrive in a per-wave LDS ring by direct global->LDS loads, NX-1
+// Per 32-point block and wave (point rows 0..31 of the block):
+//   x rows   arrive in a per-wave LDS ring by direct global->LDS copies, two
 //            blocks ahead of use; they never pass through registers.
 //   logits   L[m][p] = W2'[:, h*M+m] . x[p] + b2'   16x16x32 MFMA, A = W2'^T
 //            fragments, B = x^T read from the ring; W2' = W2 * log2(e)/tau so
-//            the softmax uses exp2.  Lane (g, p) holds slices 16*mt + 4*g + r.
+//            the softmax uses exp2.  Lane (g, li) of point tile pt holds
+//            slices 16*mt + 4*g + r of point row prow(pt, li).
 //   softmax  over the M slices of each point: in-lane, then two cross-row swaps.
-//   w rows   normalised and written to a per-wave LDS tile (two tiles, so
-//            block b's softmax can run while block b-1 is contracted).
+//   w rows   normalised and written to a per-wave LDS tile.
 //   contract S[m][c] += sum_p w[p][m] x[p][c] (A = w^T, B = x) and
 //            d[m] += sum_p w[p][m] (A = w^T against a ones operand), with
 //            ds_read_b64_tr_b16 giving operands whose K slots hold points:
-//            slot (g, t) <-> point 8g+t.
-// With bf16 storage block b-1's contraction (matrix cores) is interleaved with
-// block b's softmax (vector ALU); fp32 storage, the parity path, runs the
-// steps of a block back to back.
+//            slot (g, t) <-> point row 8g+t.
+// With bf16 storage the block loop is unrolled by the ring depth (every tile
+// address is then a fixed per-lane offset plus an immediate), and block b-1's
+// contraction (matrix cores) is interleaved with block b's softmax (vector
+// ALU).  fp32 storage, the parity path, runs the steps of a block back to back.
 #pragma once
+#include <type_traits>
 #include "ts3_device.h"
 
 namespace ts3 {
@@ -42,38 +44,43 @@ template <typename T, int C, int M> struct Pass1Cfg {
     static constexpr int WROW = M * (int)sizeof(T);    // bytes per point row of w
     static constexpr int XTILE = 32 * XROW;
     static constexpr int WTILE = 32 * WROW;
-    static constexpr int NX = PIPE ? 3 : 1;            // x ring depth
-    static constexpr int NW = PIPE ? 2 : 1;            // w tiles
-    static constexpr int ROWS_PER_LOAD = 1024 / XROW;  // rows per 1 KB wave load
-    static constexpr int LOADS = 32 / ROWS_PER_LOAD;   // wave loads per block
-    static constexpr int WAVE_BYTES = NX * XTILE + NW * WTILE;
+    static constexpr int NS = PIPE ? 3 : 1;            // ring depth (x and w tiles)
+    static constexpr int ROWS_PER_LOAD = 1024 / XROW;  // rows per 1 KB wave copy
+    static constexpr int LOADS = 32 / ROWS_PER_LOAD;   // wave copies per block
+    static constexpr int WAVE_BYTES = NS * (XTILE + WTILE);
     static constexpr int XT_BYTES = WAVES * WAVE_BYTES;
     static constexpr int RED_BYTES = WAVES * M * (C + 1) * 4;
     static constexpr int LDS_BYTES = XT_BYTES > RED_BYTES ? XT_BYTES : RED_BYTES;
-    static_assert(ROWS_PER_LOAD * XROW == 1024, "x rows must tile a 1 KB load");
+    static_assert(ROWS_PER_LOAD * XROW == 1024, "x rows must tile a 1 KB copy");
 };
 
-// Bank-conflict-free placement inside unpadded tile rows.
-// x rows (16-byte chunks): chunk k of row R sits at k ^ xswz(R).  Each group of
-// eight consecutive rows sees all eight values mod 8, so 8-lane phases of
-// 16-byte accesses to consecutive rows hit distinct banks, and a 16-lane
-// transpose read (rows 8g+q, q < 4, two chunks) sees 2q in bits 1-2.
+// Point row of lane li in point tile pt: bits 0-1 from li, bit 2 from pt,
+// bits 3-4 from li >> 2.  The eight lanes of a 16-byte access phase then cover
+// rows that differ in bits 0, 1 and 3, and a transpose read's lower and upper
+// four rows (bit 2) share one swizzle.
+__device__ __forceinline__ int prow(int pt, int li) { return (li & 3) | (pt << 2) | ((li >> 2) << 3); }
+
+// Bank-conflict-free placement inside unpadded tile rows (none depends on row
+// bit 2, so rows r and r+4 differ by a fixed offset).
+// x rows (16-byte chunks): chunk k of row R sits at k ^ xswz(R).  Over row
+// bits 0, 1 and 3 it takes all eight values mod 8, so 16-byte reads of eight
+// such rows hit distinct banks, and a 16-lane transpose read (rows 8g+q, q < 4,
+// two chunks) sees 2q in bits 1-2.
 template <int ROWB> __device__ __forceinline__ int xswz(int R) {
     constexpr int NCH = ROWB / 16;
-    const int f = (2 * (R & 3)) ^ ((R >> 2) & 1) ^ (NCH >= 16 ? ((R >> 3) & 1) << 3 : 0);
-    return f & (NCH - 1);
+    return ((2 * (R & 3)) ^ ((R >> 3) & 1)) & (NCH - 1);
 }
 template <int ROWB> __device__ __forceinline__ int xoff(int R, int byte) {
     return R * ROWB + (((byte >> 4) ^ xswz<ROWB>(R)) << 4) + (byte & 15);
 }
 // w rows (8-byte slots): slot s of row R sits at s ^ wswz(R), chosen per row
-// width so that the sixteen rows of an 8-byte store phase and the four rows x
-// four slots of a transpose read cover distinct banks.
+// width so that the sixteen rows of an 8-byte store phase (row bits 0, 1, 3, 4)
+// and the four rows x four slots of a transpose read cover distinct banks.
 template <int ROWB> __device__ __forceinline__ int wswz(int R) {
-    constexpr int NS = ROWB / 8;
-    if constexpr (NS >= 16) return ((R & 3) << 2) | ((R >> 2) & 3);
-    else if constexpr (NS == 8) return (((R >> 1) & 1) << 2) | ((R >> 2) & 3);
-    else return ((R >> 2) & 3) & (NS - 1);
+    constexpr int NSL = ROWB / 8;
+    if constexpr (NSL >= 16) return ((R & 3) << 2) | ((R >> 3) & 3);
+    else if constexpr (NSL == 8) return (((R >> 1) & 1) << 2) | ((R >> 3) & 3);
+    else return ((R >> 3) & 3) & (NSL - 1);
 }
 template <int ROWB> __device__ __forceinline__ int woff(int R, int byte) {
     return R * ROWB + (((byte >> 3) ^ wswz<ROWB>(R)) << 3) + (byte & 7);
@@ -85,29 +92,33 @@ typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 // One 8-slot operand fragment from two transposing LDS reads.  Lane (g, j) of
 // each 16-lane row reads row 8g + 4*half + j/4, columns col0 + 4*(j%4) .. +3 of
 // a tile; the result gives lane (g, i) column col0 + i of rows 8g .. 8g+7 in
-// slots 0..7.  OFF maps (row, logical byte) to the tile's swizzled offset.
+// slots 0..7.  `lo` is the lane's address for half 0; half 1 is 4 rows on.
+template <int ROWB>
+__device__ __forceinline__ void tr_frag(Frag<bf16_t> &f, const unsigned char *lo) {
+    const s16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)lo);
+    const s16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(lo + 4 * ROWB));
+    typedef short s16x8 __attribute__((ext_vector_type(8)));
+    const s16x8 v = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+    f.v = __builtin_bit_cast(bf16x8, v);
+}
 template <int ROWB, bool XT>
-__device__ __forceinline__ void tr_frag(Frag<bf16_t> &f, const unsigned char *base, int g, int col0, int j) {
+__device__ __forceinline__ const unsigned char *tr_addr(const unsigned char *tile, int g, int col0, int j) {
     const int r = 8 * g + (j >> 2);
     const int byte = (col0 + 4 * (j & 3)) * 2;
-    const int o0 = XT ? xoff<ROWB>(r, byte) : woff<ROWB>(r, byte);
-    const int o1 = XT ? xoff<ROWB>(r + 4, byte) : woff<ROWB>(r + 4, byte);
-    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(base + o0));
-    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(base + o1));
-    typedef short s16x8 __attribute__((ext_vector_type(8)));
-    const s16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-    f.v = __builtin_bit_cast(bf16x8, v);
+    return tile + (XT ? xoff<ROWB>(r, byte) : woff<ROWB>(r, byte));
 }
 // fp32 tiles: the same fragment read element by element (fp32 storage is the
 // parity path, not the fast one).
 template <int ROWB, bool XT>
-__device__ __forceinline__ void tr_frag(Frag<float> &f, const unsigned char *base, int g, int col0, int i) {
+__device__ __forceinline__ void tr_frag_f32(Frag<float> &f, const unsigned char *tile, int g, int col0, int i) {
 #pragma unroll
     for (int t = 0; t < 8; ++t) {
         const int o = XT ? xoff<ROWB>(8 * g + t, (col0 + i) * 4) : woff<ROWB>(8 * g + t, (col0 + i) * 4);
-        f.v[t] = *reinterpret_cast<const float *>(base + o);
+        f.v[t] = *reinterpret_cast<const float *>(tile + o);
     }
 }
+
+template <int V> using ic = std::integral_constant<int, V>;
 
 // x       : tile base, [n_tile][C] storage elements
 // n_tile  : points in this tile (tile starts on a span boundary)
@@ -123,7 +134,8 @@ __global__ __launch_bounds__(256, 1) void k_slice_accumulate(
     const T *__restrict__ w2p, const float *__restrict__ b2s, float *__restrict__ partials) {
     using Cfg = Pass1Cfg<T, C, M>;
     constexpr int CT = Cfg::CT, MT = Cfg::MT, CK = Cfg::CK;
-    constexpr int XROW = Cfg::XROW, WROW = Cfg::WROW, NX = Cfg::NX, NW = Cfg::NW;
+    constexpr int XROW = Cfg::XROW, WROW = Cfg::WROW, NS = Cfg::NS;
+    constexpr int XTILE = Cfg::XTILE, WTILE = Cfg::WTILE;
     __shared__ __attribute__((aligned(1024))) unsigned char lds[Cfg::LDS_BYTES];
 
     const int nwg = nspan * H;
@@ -131,7 +143,7 @@ __global__ __launch_bounds__(256, 1) void k_slice_accumulate(
     const int span_local = jwg / H;
     const int h = jwg - span_local * H;
     const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     const int li = lane & 15;
     const int g = lane >> 4;
 
@@ -140,27 +152,38 @@ __global__ __launch_bounds__(256, 1) void k_slice_accumulate(
     const int nblk = (int)((p_end - p_begin + 31) >> 5);
     const int nmine = nblk > wave ? (nblk - wave + Cfg::WAVES - 1) / Cfg::WAVES : 0;
 
-    unsigned char *wave_lds = lds + wave * Cfg::WAVE_BYTES;
-    auto xslot = [&](int j) { return wave_lds + (j % NX) * Cfg::XTILE; };
-    auto wslot = [&](int j) { return wave_lds + NX * Cfg::XTILE + (j % NW) * Cfg::WTILE; };
+    unsigned char *const wave_lds = lds + wave * Cfg::WAVE_BYTES;
+    unsigned char *const xring = wave_lds;                // NS x tiles
+    unsigned char *const wring = wave_lds + NS * XTILE;   // NS w tiles
+    const uint32_t xring_lds = lds_addr(xring);
 
-    // Block j of this wave (mesh block wave + 4j) into x slot j % NX.  Lane l of
-    // load i fills physical chunk l % NCH of row i*ROWS_PER_LOAD + l / NCH, so it
-    // reads the logical chunk stored there.  Rows past the span's end repeat
-    // its last point (finite data that the zero weights of padding points
-    // cancel exactly), which also keeps every wave's load count uniform.
-    auto issue_x = [&](int j) {
-        constexpr int NCH = XROW / 16;
-        unsigned char *slot = xslot(j);
+    // Block j of this wave (mesh block wave + 4j) into x slot SL.  Lane l of
+    // copy i fills physical chunk l % NCH of row i*ROWS_PER_LOAD + l / NCH, so
+    // it reads the logical chunk stored there.  Rows past the span's end
+    // repeat its last point (finite data that the zero weights of padding
+    // points cancel exactly), which also keeps every wave's copy count uniform.
+    constexpr int NCH = XROW / 16;
+    auto copy_off = [&](int i) {
+        const int R = i * Cfg::ROWS_PER_LOAD + lane / NCH;
+        return (uint32_t)(R * XROW + (((lane % NCH) ^ xswz<XROW>(R)) << 4));
+    };
+    auto issue_x = [&](int j, auto slot) {
+        constexpr int SL = decltype(slot)::value;
         const int64_t p0 = p_begin + ((int64_t)(wave + Cfg::WAVES * j) << 5);
+        const uint32_t dst = xring_lds + SL * XTILE;
+        if (p0 + 32 <= p_end) {
+            const void *base = x + p0 * C;
 #pragma unroll
-        for (int i = 0; i < Cfg::LOADS; ++i) {
-            const int R = i * Cfg::ROWS_PER_LOAD + lane / NCH;
-            const int k = (lane % NCH) ^ xswz<XROW>(R);
-            int64_t p = p0 + R;
-            p = p < p_end ? p : p_end - 1;
-            const unsigned char *src = reinterpret_cast<const unsigned char *>(x + (size_t)p * C) + k * 16;
-            dma16(src, lds_addr(slot + i * 1024));
+            for (int i = 0; i < Cfg::LOADS; ++i) dma16s<0>(copy_off(i), base, dst + i * 1024);
+        } else {
+#pragma unroll
+            for (int i = 0; i < Cfg::LOADS; ++i) {
+                const int R = i * Cfg::ROWS_PER_LOAD + lane / NCH;
+                const int k = (lane % NCH) ^ xswz<XROW>(R);
+                int64_t p = p0 + R;
+                p = p < p_end ? p : p_end - 1;
+                dma16(reinterpret_cast<const unsigned char *>(x + (size_t)p * C) + k * 16, dst + i * 1024);
+            }
         }
     };
 
@@ -192,47 +215,51 @@ __global__ __launch_bounds__(256, 1) void k_slice_accumulate(
     // assume its own copies are the only memory operations in flight.
     wait_vmcnt<0>();
 
-    // Logits B operand from x slot j: lane (g, li) holds point 16*pt + li,
-    // channels 32*kc + 8*g .. +8.
-    auto read_x = [&](int j, Frag<T> (&xb)[2][CK]) {
-        const unsigned char *src = xslot(j);
+    // Logits for the block in x slot SL: L[mt][pt] lane (g, li) holds slices
+    // 16*mt + 4*g .. +3 of point row prow(pt, li).  The B operand (channels
+    // 32*kc + 8*g .. +8 of that row) is read just before use.
+    auto logits = [&](auto slot, f32x4 (&L)[MT][2]) {
+        constexpr int SL = decltype(slot)::value;
+        const unsigned char *tile = xring + SL * XTILE;
 #pragma unroll
-        for (int pt = 0; pt < 2; ++pt)
+        for (int pt = 0; pt < 2; ++pt) {
+            const int R = prow(pt, li);
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) L[mt][pt] = bias[mt];
 #pragma unroll
             for (int kc = 0; kc < CK; ++kc) {
-                const int R = pt * 16 + li, byte = (kc * 32 + g * 8) * (int)sizeof(T);
+                const int byte = (kc * 32 + g * 8) * (int)sizeof(T);
+                Frag<T> xb;
                 if constexpr (sizeof(T) == 2) {
-                    xb[pt][kc].v = *reinterpret_cast<const bf16x8 *>(src + xoff<XROW>(R, byte));
+                    xb.v = *reinterpret_cast<const bf16x8 *>(tile + xoff<XROW>(R, byte));
                 } else {
-                    const float4 a = *reinterpret_cast<const float4 *>(src + xoff<XROW>(R, byte));
-                    const float4 b = *reinterpret_cast<const float4 *>(src + xoff<XROW>(R, byte + 16));
-                    xb[pt][kc].v[0] = a.x; xb[pt][kc].v[1] = a.y; xb[pt][kc].v[2] = a.z; xb[pt][kc].v[3] = a.w;
-                    xb[pt][kc].v[4] = b.x; xb[pt][kc].v[5] = b.y; xb[pt][kc].v[6] = b.z; xb[pt][kc].v[7] = b.w;
+                    const float4 a = *reinterpret_cast<const float4 *>(tile + xoff<XROW>(R, byte));
+                    const float4 b = *reinterpret_cast<const float4 *>(tile + xoff<XROW>(R, byte + 16));
+                    xb.v[0] = a.x; xb.v[1] = a.y; xb.v[2] = a.z; xb.v[3] = a.w;
+                    xb.v[4] = b.x; xb.v[5] = b.y; xb.v[6] = b.z; xb.v[7] = b.w;
                 }
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) mma(L[mt][pt], w2[mt][kc], xb);
             }
+        }
     };
-    auto logits = [&](const Frag<T> (&xb)[2][CK], f32x4 (&L)[MT][2]) {
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-            for (int pt = 0; pt < 2; ++pt) {
-                L[mt][pt] = bias[mt];
-#pragma unroll
-                for (int kc = 0; kc < CK; ++kc) mma(L[mt][pt], w2[mt][kc], xb[pt][kc]);
-            }
-    };
-    // S += w^T x, d += sum_p w for block j (x slot j % NX, w tile j % NW).
-    auto contract = [&](int j) {
-        const unsigned char *xt = xslot(j), *wt = wslot(j);
+    // S += w^T x, d += sum_p w for the block in slot SL.
+    auto contract = [&](auto slot) {
+        constexpr int SL = decltype(slot)::value;
+        const unsigned char *xt = xring + SL * XTILE, *wt = wring + SL * WTILE;
         Frag<T> a[MT];
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) tr_frag<WROW, false>(a[mt], wt, g, mt * 16, li);
+        for (int mt = 0; mt < MT; ++mt) {
+            if constexpr (sizeof(T) == 2) tr_frag<WROW>(a[mt], tr_addr<WROW, false>(wt, g, mt * 16, li));
+            else tr_frag_f32<WROW, false>(a[mt], wt, g, mt * 16, li);
+        }
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) mma(D[mt], a[mt], ones);
 #pragma unroll
         for (int ct = 0; ct < CT; ++ct) {
             Frag<T> b;
-            tr_frag<XROW, true>(b, xt, g, ct * 16, li);
+            if constexpr (sizeof(T) == 2) tr_frag<XROW>(b, tr_addr<XROW, true>(xt, g, ct * 16, li));
+            else tr_frag_f32<XROW, true>(b, xt, g, ct * 16, li);
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) mma(S[mt][ct], a[mt], b);
         }
@@ -254,7 +281,7 @@ __global__ __launch_bounds__(256, 1) void k_slice_accumulate(
                 }
             sum = xrow_sum(sum);
             ok = ok && softmax_sum_ok(sum);
-            inv[pt] = (pt * 16 + li < valid) ? fast_rcp(sum) : 0.f;
+            inv[pt] = prow(pt, li) < valid ? fast_rcp(sum) : 0.f;
         }
         return ok;
     };
@@ -276,27 +303,28 @@ __global__ __launch_bounds__(256, 1) void k_slice_accumulate(
                     L[mt][pt][r] = e;
                     sum += e;
                 }
-            inv[pt] = (pt * 16 + li < valid) ? fast_rcp(xrow_sum(sum)) : 0.f;
+            inv[pt] = prow(pt, li) < valid ? fast_rcp(xrow_sum(sum)) : 0.f;
         }
     };
-    // Normalised w rows into w tile j % NW: lane (g, li) stores slices
-    // 16*mt + 4*g .. +3 of point 16*pt + li.
-    auto store_w = [&](int j, const f32x4 (&E)[MT][2], const float (&inv)[2]) {
-        unsigned char *dst = wslot(j);
+    // Normalised w rows into w slot SL: lane (g, li) stores slices
+    // 16*mt + 4*g .. +3 of point row prow(pt, li).
+    auto store_w = [&](auto slot, const f32x4 (&E)[MT][2], const float (&inv)[2]) {
+        constexpr int SL = decltype(slot)::value;
+        unsigned char *tile = wring + SL * WTILE;
 #pragma unroll
         for (int pt = 0; pt < 2; ++pt)
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
-                const int R = pt * 16 + li, byte = (mt * 16 + g * 4) * (int)sizeof(T);
+                const int R = prow(pt, li), byte = (mt * 16 + g * 4) * (int)sizeof(T);
                 const float a0 = E[mt][pt][0] * inv[pt], a1 = E[mt][pt][1] * inv[pt];
                 const float a2 = E[mt][pt][2] * inv[pt], a3 = E[mt][pt][3] * inv[pt];
                 if constexpr (sizeof(T) == 2) {
                     typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
-                    *reinterpret_cast<bf16x4 *>(dst + woff<WROW>(R, byte)) =
+                    *reinterpret_cast<bf16x4 *>(tile + woff<WROW>(R, byte)) =
                         bf16x4{(__bf16)a0, (__bf16)a1, (__bf16)a2, (__bf16)a3};
                 } else {
-                    *reinterpret_cast<float2 *>(dst + woff<WROW>(R, byte)) = float2{a0, a1};
-                    *reinterpret_cast<float2 *>(dst + woff<WROW>(R, byte + 8)) = float2{a2, a3};
+                    *reinterpret_cast<float2 *>(tile + woff<WROW>(R, byte)) = float2{a0, a1};
+                    *reinterpret_cast<float2 *>(tile + woff<WROW>(R, byte + 8)) = float2{a2, a3};
                 }
             }
     };
@@ -306,65 +334,179 @@ __global__ __launch_bounds__(256, 1) void k_slice_accumulate(
     };
 
     if constexpr (Cfg::PIPE) {
-        // The tiles of "block -1" hold zeros, so the first iteration's
-        // contraction of the previous block adds exactly nothing.
-        {
-            uint4 *zx = reinterpret_cast<uint4 *>(xslot(NX - 1));
-            uint4 *zw = reinterpret_cast<uint4 *>(wslot(NW - 1));
-            for (int i = lane; i < Cfg::XTILE / 16; i += 64) zx[i] = uint4{0u, 0u, 0u, 0u};
-            for (int i = lane; i < Cfg::WTILE / 16; i += 64) zw[i] = uint4{0u, 0u, 0u, 0u};
-        }
+        // bf16 tile addresses as (per-lane base) ^ (tile-index constant) +
+        // (immediate): with 16-bit elements a tile step moves whole chunks or
+        // slots whose index bits do not overlap the base's, and neither
+        // swizzle depends on row bit 2 (point tile pt, transpose half).
+        static_assert(sizeof(T) == 2, "the pipelined path is written for 16-bit storage");
+        const uint32_t wave_off = (uint32_t)(wave * Cfg::WAVE_BYTES);
+        uint32_t xl0 = wave_off + xoff<XROW>(prow(0, li), 16 * g);               // logits B, kc = 0
+        uint32_t xt0 = wave_off + xoff<XROW>(8 * g + (li >> 2), 8 * (li & 3));   // x^T, ct = 0
+        uint32_t wt0 = wave_off + NS * XTILE + woff<WROW>(8 * g + (li >> 2), 8 * (li & 3));  // w^T, mt = 0
+        uint32_t ws0 = wave_off + NS * XTILE + woff<WROW>(prow(0, li), 8 * g);   // w rows, mt = 0
+        constexpr int PT_X = 4 * XROW, PT_W = 4 * WROW;  // row + 4
+
+        // Logits of point tile pt for the block in x slot SL.
+        auto logits16 = [&](auto slot, int pt, f32x4 (&L)[MT][2]) {
+            constexpr int SL = decltype(slot)::value;
 #pragma unroll
-        for (int j = 0; j < NX - 1; ++j) issue_x(j);
-        for (int j = 0; j < nmine; ++j) {
+            for (int mt = 0; mt < MT; ++mt) L[mt][pt] = bias[mt];
+#pragma unroll
+            for (int kc = 0; kc < CK; ++kc) {
+                Frag<T> xb;
+                xb.v = *reinterpret_cast<const bf16x8 *>(lds + (xl0 ^ (kc << 6)) + SL * XTILE + pt * PT_X);
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) mma(L[mt][pt], w2[mt][kc], xb);
+            }
+        };
+        // Contraction operands of the block in slot SL: w^T for every slice
+        // tile, x^T for channel tile ct.
+        auto read_a = [&](auto slot, Frag<T> (&a)[MT]) {
+            constexpr int SL = decltype(slot)::value;
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) tr_frag<WROW>(a[mt], lds + (wt0 ^ (mt << 5)) + SL * WTILE);
+        };
+        auto read_b = [&](auto slot, int ct, Frag<T> &b) {
+            constexpr int SL = decltype(slot)::value;
+            tr_frag<XROW>(b, lds + (xt0 ^ (ct << 5)) + SL * XTILE);
+        };
+        auto contract16 = [&](auto slot) {
+            Frag<T> a[MT], b;
+            read_a(slot, a);
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) mma(D[mt], a[mt], ones);
+#pragma unroll
+            for (int ct = 0; ct < CT; ++ct) {
+                read_b(slot, ct, b);
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) mma(S[mt][ct], a[mt], b);
+            }
+        };
+        auto store_w16 = [&](auto slot, const f32x4 (&E)[MT][2], const float (&inv)[2]) {
+            constexpr int SL = decltype(slot)::value;
+            typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
+#pragma unroll
+            for (int pt = 0; pt < 2; ++pt)
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+                    *reinterpret_cast<bf16x4 *>(lds + (ws0 ^ (mt << 5)) + SL * WTILE + pt * PT_W) =
+                        bf16x4{(__bf16)(E[mt][pt][0] * inv[pt]), (__bf16)(E[mt][pt][1] * inv[pt]),
+                               (__bf16)(E[mt][pt][2] * inv[pt]), (__bf16)(E[mt][pt][3] * inv[pt])};
+        };
+        // exp2 of point tile pt's logits in place; returns the in-lane sum.
+        auto exp_tile = [&](f32x4 (&L)[MT][2], int pt) {
+            float sum = 0.f;
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const float e = fast_exp2(L[mt][pt][r]);
+                    L[mt][pt][r] = e;
+                    sum += e;
+                }
+            return sum;
+        };
+
+        // One block j in slot SL = j % NS, overlapping three streams:
+        //   logits of point tile 0, then of tile 1 beside tile 0's exp2;
+        //   the previous block's contraction beside tile 1's exp2, the
+        //   normalisation and this block's w rows;
+        //   then the copy of block j + NS - 1 into the slot just freed.
+        auto step = [&](int j, auto slot) {
+            constexpr int SL = decltype(slot)::value;
+            constexpr int PREV = (SL + NS - 1) % NS;
+            // Keep the derived addresses inside the step (recomputed with one
+            // XOR each) instead of occupying registers across the loop.
+            asm volatile("" : "+v"(xl0), "+v"(xt0), "+v"(wt0), "+v"(ws0));
             const int valid = block_valid(j);
-            wait_vmcnt<(NX - 2) * Cfg::LOADS>();  // block j's rows have landed
+            Frag<T> a[MT], b;
+            read_a(ic<PREV>{}, a);  // the previous block's tiles are complete
+            read_b(ic<PREV>{}, 0, b);
+            wait_vmcnt<(NS - 2) * Cfg::LOADS>();  // block j's rows have landed
             asm volatile("" ::: "memory");
-            Frag<T> xb[2][CK];
-            read_x(j, xb);
             f32x4 L[MT][2];
-            logits(xb, L);
+            logits16(slot, 0, L);
             __builtin_amdgcn_sched_barrier(0);
-            // Block j-1's contraction (matrix cores) interleaved with block j's
-            // softmax and w rows (vector ALU).
-            contract(j - 1 + NX * NW);
-            float inv[2];
-            const bool ok = softmax_fast(L, inv, valid);
-            store_w(j, L, inv);
-            interleave_mfma_valu<MT * (CT + 1), 4, 2>();
+            logits16(slot, 1, L);
+            float sum0 = exp_tile(L, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, CK, 0);
+#pragma unroll
+            for (int i = 0; i < MT * CK; ++i) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) mma(D[mt], a[mt], ones);
+#pragma unroll
+            for (int ct = 0; ct < CT; ++ct) {
+                Frag<T> bn;
+                if (ct + 1 < CT) read_b(ic<PREV>{}, ct + 1, bn);
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) mma(S[mt][ct], a[mt], b);
+                b = bn;
+            }
+            float sum1 = exp_tile(L, 1);
+            sum0 = xrow_sum(sum0);
+            sum1 = xrow_sum(sum1);
+            const bool ok = softmax_sum_ok(sum0) && softmax_sum_ok(sum1);
+            float inv[2] = {prow(0, li) < valid ? fast_rcp(sum0) : 0.f, prow(1, li) < valid ? fast_rcp(sum1) : 0.f};
+            store_w16(slot, L, inv);
+            interleave_chain<0, MT * (CT + 1), 5, MT - 1, MT, 2, 2 * MT>();
             __builtin_amdgcn_sched_barrier(0);
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-            issue_x(j - 1 + NX);  // block j-1's x slot is free again
+            issue_x(j + NS - 1, ic<PREV>{});
             if (__any(!ok)) {
                 // Rare: some row's exp2 sum left the safe window; redo the
                 // block with the max shift.
-                read_x(j, xb);
-                logits(xb, L);
+                logits16(slot, 0, L);
+                logits16(slot, 1, L);
                 softmax_shifted(L, inv, valid);
-                store_w(j, L, inv);
+                store_w16(slot, L, inv);
             }
             asm volatile("" ::: "memory");
+        };
+        // The tiles of "block -1" (slot NS-1) hold zeros, so the first step's
+        // contraction of the previous block adds exactly nothing.
+        {
+            uint4 *zx = reinterpret_cast<uint4 *>(xring + (NS - 1) * XTILE);
+            uint4 *zw = reinterpret_cast<uint4 *>(wring + (NS - 1) * WTILE);
+            for (int i = lane; i < XTILE / 16; i += 64) zx[i] = uint4{0u, 0u, 0u, 0u};
+            for (int i = lane; i < WTILE / 16; i += 64) zw[i] = uint4{0u, 0u, 0u, 0u};
         }
+        static_assert(NS == 3, "the unrolled loop below assumes a ring of three");
+        issue_x(0, ic<0>{});
+        issue_x(1, ic<1>{});
+        int j = 0;
+        for (; j + 3 <= nmine; j += 3) {
+            step(j, ic<0>{});
+            step(j + 1, ic<1>{});
+            step(j + 2, ic<2>{});
+        }
+        if (j < nmine) step(j, ic<0>{});
+        if (j + 1 < nmine) step(j + 1, ic<1>{});
         wait_vmcnt<0>();
-        contract(nmine - 1 + NX * NW);  // the last block
+        switch ((nmine + NS - 1) % NS) {  // the last block (slot 2 if there was none)
+            case 0: contract16(ic<0>{}); break;
+            case 1: contract16(ic<1>{}); break;
+            default: contract16(ic<2>{}); break;
+        }
     } else {
         for (int j = 0; j < nmine; ++j) {
             const int valid = block_valid(j);
-            issue_x(j);
+            issue_x(j, ic<0>{});
             wait_vmcnt<0>();
             asm volatile("" ::: "memory");
-            Frag<T> xb[2][CK];
-            read_x(j, xb);
             f32x4 L[MT][2];
-            logits(xb, L);
+            logits(ic<0>{}, L);
             float inv[2];
             if (__any(!softmax_fast(L, inv, valid))) {
-                logits(xb, L);
+                logits(ic<0>{}, L);
                 softmax_shifted(L, inv, valid);
             }
-            store_w(j, L, inv);
+            store_w(ic<0>{}, L, inv);
             asm volatile("" ::: "memory");
-            contract(j);
+            contract(ic<0>{});
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
         }
     }
