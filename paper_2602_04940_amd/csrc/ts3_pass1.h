@@ -55,32 +55,39 @@ template <typename T, int C, int M> struct Pass1Cfg {
 };
 
 // Point row of lane li in point tile pt: bits 0-1 from li, bit 2 from pt,
-// bits 3-4 from li >> 2.  The eight lanes of a 16-byte access phase then cover
-// rows that differ in bits 0, 1 and 3, and a transpose read's lower and upper
-// four rows (bit 2) share one swizzle.
+// bits 3-4 from li >> 2, so point tiles 0 and 1 differ only in row bit 2.
 __device__ __forceinline__ int prow(int pt, int li) { return (li & 3) | (pt << 2) | ((li >> 2) << 3); }
 
-// Bank-conflict-free placement inside unpadded tile rows (none depends on row
-// bit 2, so rows r and r+4 differ by a fixed offset).
-// x rows (16-byte chunks): chunk k of row R sits at k ^ xswz(R).  Over row
-// bits 0, 1 and 3 it takes all eight values mod 8, so 16-byte reads of eight
-// such rows hit distinct banks, and a 16-lane transpose read (rows 8g+q, q < 4,
-// two chunks) sees 2q in bits 1-2.
+// Bank-conflict-free placement inside unpadded tile rows.  The LDS serves
+// 256 bytes per cycle (64 banks of 4 bytes): a 16-byte access is served in
+// phases of 16 lanes and an 8-byte access in phases of 32 lanes, and a phase
+// is conflict-free when its lanes touch distinct banks.  No swizzle below
+// depends on row bit 2, so rows r and r+4 (point tile pt, transpose half)
+// differ by a fixed offset; with 16-bit elements a step of the channel, slice
+// or K index then changes the offset by an XOR with a constant.
+// x rows (16-byte chunks): chunk k of row R sits at k ^ xswz(R).  A logits
+// read phase covers rows differing in bits 0, 1, 3, 4, a transpose-read phase
+// rows differing in bits 0, 1, 3 with two chunks each; both land on 16
+// distinct chunk positions per 256 bytes.
 template <int ROWB> __device__ __forceinline__ int xswz(int R) {
     constexpr int NCH = ROWB / 16;
-    return ((2 * (R & 3)) ^ ((R >> 3) & 1)) & (NCH - 1);
+    const int b0 = R & 1, b1 = (R >> 1) & 1, b3 = (R >> 3) & 1, b4 = (R >> 4) & 1;
+    const int f = NCH >= 16 ? (b4 | (b0 << 1) | (b1 << 2) | (b3 << 3)) : (b4 | (b1 << 1) | (b3 << 2));
+    return f & (NCH - 1);
 }
 template <int ROWB> __device__ __forceinline__ int xoff(int R, int byte) {
     return R * ROWB + (((byte >> 4) ^ xswz<ROWB>(R)) << 4) + (byte & 15);
 }
 // w rows (8-byte slots): slot s of row R sits at s ^ wswz(R), chosen per row
-// width so that the sixteen rows of an 8-byte store phase (row bits 0, 1, 3, 4)
-// and the four rows x four slots of a transpose read cover distinct banks.
+// width so that the 32 lanes of an 8-byte store phase (rows differing in bits
+// 0, 1, 3, 4) and of a transpose-read phase (four rows x four slots x two row
+// groups) touch distinct banks (with 32-byte rows, M = 16, two-way at worst).
 template <int ROWB> __device__ __forceinline__ int wswz(int R) {
     constexpr int NSL = ROWB / 8;
-    if constexpr (NSL >= 16) return ((R & 3) << 2) | ((R >> 3) & 3);
-    else if constexpr (NSL == 8) return (((R >> 1) & 1) << 2) | ((R >> 3) & 3);
-    else return ((R >> 3) & 3) & (NSL - 1);
+    const int b1 = (R >> 1) & 1, b3 = (R >> 3) & 1, b4 = (R >> 4) & 1;
+    if constexpr (NSL >= 16) return (b4 << 1) | (b1 << 2) | (b3 << 3);
+    else if constexpr (NSL == 8) return (b4 << 1) | (b3 << 2);
+    else return (b3 | (b4 << 1)) & (NSL - 1);
 }
 template <int ROWB> __device__ __forceinline__ int woff(int R, int byte) {
     return R * ROWB + (((byte >> 3) ^ wswz<ROWB>(R)) << 3) + (byte & 7);
