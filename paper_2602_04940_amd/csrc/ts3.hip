@@ -84,24 +84,26 @@ hipError_t launch_pass2(const void *x, int64_t n, int32_t H, const void *w2p, co
     using Cfg = Pass2Cfg<T, C, M>;
     const int64_t nblk = (n + Cfg::POINTS_PER_WG - 1) / Cfg::POINTS_PER_WG;
     if constexpr (sizeof(T) == 2) {
-        const size_t lds = Pass2LdsCfg<T, C, M>::lds_bytes(H);
+        using WCfg = Pass2W8Cfg<T, C, M>;
+        const size_t lds = WCfg::lds_bytes(H);
         static size_t static_lds = SIZE_MAX;
         if (static_lds == SIZE_MAX) {
             hipFuncAttributes fa{};
-            static_lds = hipFuncGetAttributes(&fa, (const void *)k_deslice_lds<T, C, M>) == hipSuccess
+            static_lds = hipFuncGetAttributes(&fa, (const void *)k_deslice_w8<T, C, M>) == hipSuccess
                              ? fa.sharedSizeBytes : PASS2_LDS_MAX;
         }
         static size_t dyn_set = 0;  // dynamic LDS limit granted so far
         if (lds + static_lds <= PASS2_LDS_MAX) {
             if (lds > dyn_set) {
-                if (hipFuncSetAttribute((const void *)k_deslice_lds<T, C, M>,
+                if (hipFuncSetAttribute((const void *)k_deslice_w8<T, C, M>,
                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
                     return hipGetLastError();
                 dyn_set = lds;
             }
-            const int64_t grid = std::min<int64_t>(nblk, device_cu_count());
-            hipLaunchKernelGGL((k_deslice_lds<T, C, M>), dim3((unsigned)grid), dim3(256), lds, st, (const T *)x,
-                               n, H, (const T *)w2p, b2s, (const T *)zp, b3, (T *)out);
+            const int64_t wblk = (n + WCfg::POINTS_PER_WG - 1) / WCfg::POINTS_PER_WG;
+            const int64_t grid = std::min<int64_t>(wblk, device_cu_count());
+            hipLaunchKernelGGL((k_deslice_w8<T, C, M>), dim3((unsigned)grid), dim3(64 * WCfg::WAVES), lds, st,
+                               (const T *)x, n, H, (const T *)w2p, b2s, (const T *)zp, b3, (T *)out);
             return hipSuccess;
         }
     }

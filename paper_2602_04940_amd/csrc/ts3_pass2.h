@@ -3,9 +3,8 @@
 // recomputed from x and never stored:
 //     out[p] = sum_h sum_m softmax_m(L_h[p]) Z[h][m][:] + b3.
 //
-// Work decomposition: each wave decodes a block of 16*PT points over all
-// heads, so the sum over heads stays in its accumulator registers.
-// Per head:
+// A wave decodes a block of 16*PT points over all heads, so the sum over heads
+// stays in its accumulator registers.  Per head:
 //   logits  L[m][p] = W2'[:, h*M+m] . x[p] + b2'  16x16x32 MFMA with A = W2'^T
 //           fragments, B = x^T (the wave's point rows, loaded once per block).
 //           Output lane (g, p) holds slices 4g+r of each 16-slice tile, so the
@@ -13,6 +12,9 @@
 //   deslice out[c][p] += Z[h]^T[c][m] . w[m][p]: A = prepared Z fragments
 //           whose K slots follow the logits' register order, B = w straight
 //           from registers.
+// Output channels: row i of channel tile ct of the Z fragments is channel
+// zchan(ct, i), so that output lane (g, p) of tiles 2k and 2k+1 holds the
+// eight consecutive channels 32k + 8g .. +7 of point p (one 16-byte store).
 #pragma once
 #include <type_traits>
 
@@ -20,136 +22,9 @@
 
 namespace ts3 {
 
-template <typename T, int C, int M> struct Pass2Cfg {
-    static constexpr int CT = C / 16;
-    static constexpr int MT = M / 16;
-    static constexpr int CK = C / 32;
-    static constexpr int KM = M >= 32 ? M / 32 : 1;  // K32 steps over slices (M=16 pads half a step)
-    static constexpr int PT = sizeof(T) == 2 ? 4 : 2;  // 16-point tiles per wave block
-    static constexpr int WAVES = 4;
-    static constexpr int POINTS_PER_WG = WAVES * 16 * PT;
-};
-
-// x   : [n][C] storage elements; out: [n][C]
-// w2p : prepared W2' fragments [H][MT][CK][64][8] (also the A = W2'^T layout)
-// b2s : scaled bias [H*M]
-// zp  : prepared Z fragments [H][CT][KM][64][8]
-// b3  : [C] float32
-template <typename T, int C, int M>
-__global__ __launch_bounds__(256, 1) void k_deslice(const T *__restrict__ x, int64_t n, int32_t H,
-                                                    const T *__restrict__ w2p,
-                                                    const float *__restrict__ b2s,
-                                                    const T *__restrict__ zp,
-                                                    const float *__restrict__ b3, T *__restrict__ out) {
-    using Cfg = Pass2Cfg<T, C, M>;
-    constexpr int CT = Cfg::CT, MT = Cfg::MT, CK = Cfg::CK, KM = Cfg::KM, PT = Cfg::PT;
-    const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
-    const int li = lane & 15;
-    const int g = lane >> 4;
-    const int64_t p0 = ((int64_t)blockIdx.x * Cfg::WAVES + wave) * (16 * PT);
-    if (p0 >= n) return;
-
-    // B operand x^T: lane (g, li) holds x[p0 + 16*pt + li][32*kc + 8*g .. +8].
-    Frag<T> xb[PT][CK];
-#pragma unroll
-    for (int pt = 0; pt < PT; ++pt) {
-        const int64_t p = p0 + pt * 16 + li;
-#pragma unroll
-        for (int kc = 0; kc < CK; ++kc) {
-            if (p < n)
-                load8(xb[pt][kc], x + (size_t)p * C + kc * 32 + g * 8);
-            else
-                zero8(xb[pt][kc]);
-        }
-    }
-
-    f32x4 O[CT][PT];
-#pragma unroll
-    for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-        for (int pt = 0; pt < PT; ++pt) O[ct][pt] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    for (int h = 0; h < H; ++h) {
-        f32x4 L[MT][PT];
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-            const float4 bb = *reinterpret_cast<const float4 *>(b2s + h * M + mt * 16 + g * 4);
-#pragma unroll
-            for (int pt = 0; pt < PT; ++pt) L[mt][pt] = f32x4{bb.x, bb.y, bb.z, bb.w};
-#pragma unroll
-            for (int kc = 0; kc < CK; ++kc) {
-                Frag<T> a;
-                load8(a, w2p + ((((size_t)h * MT + mt) * CK + kc) * 64 + lane) * 8);
-#pragma unroll
-                for (int pt = 0; pt < PT; ++pt) mma(L[mt][pt], a, xb[pt][kc]);
-            }
-        }
-
-        // Softmax over the head's M slices for point 16*pt + li.
-        Frag<T> wf[PT][KM];
-#pragma unroll
-        for (int pt = 0; pt < PT; ++pt) {
-            float mx = L[0][pt][0];
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) mx = fmaxf(mx, L[mt][pt][r]);
-            mx = xrow_max(mx);
-            float sum = 0.f;
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const float e = fast_exp2(L[mt][pt][r] - mx);
-                    L[mt][pt][r] = e;
-                    sum += e;
-                }
-            const float inv = fast_rcp(xrow_sum(sum));
-#pragma unroll
-            for (int km = 0; km < KM; ++km)
-#pragma unroll
-                for (int t = 0; t < 8; ++t) {
-                    const int mt = 2 * km + (t >> 2);
-                    wf[pt][km].set(t, mt < MT ? L[mt][pt][t & 3] * inv : 0.f);
-                }
-        }
-
-#pragma unroll
-        for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-            for (int km = 0; km < KM; ++km) {
-                Frag<T> a;
-                load8(a, zp + ((((size_t)h * CT + ct) * KM + km) * 64 + lane) * 8);
-#pragma unroll
-                for (int pt = 0; pt < PT; ++pt) mma(O[ct][pt], a, wf[pt][km]);
-            }
-    }
-
-    // Store: lane (g, li) holds out[p0 + 16*pt + li][16*ct + 4*g + r].
-#pragma unroll
-    for (int ct = 0; ct < CT; ++ct) {
-        const float4 bb = *reinterpret_cast<const float4 *>(b3 + ct * 16 + g * 4);
-#pragma unroll
-        for (int pt = 0; pt < PT; ++pt) {
-            const int64_t p = p0 + pt * 16 + li;
-            if (p >= n) continue;
-            const float v0 = O[ct][pt][0] + bb.x, v1 = O[ct][pt][1] + bb.y;
-            const float v2 = O[ct][pt][2] + bb.z, v3 = O[ct][pt][3] + bb.w;
-            T *dst = out + (size_t)p * C + ct * 16 + g * 4;
-            if constexpr (sizeof(T) == 2) {
-                typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
-                *reinterpret_cast<bf16x4 *>(dst) = bf16x4{(__bf16)v0, (__bf16)v1, (__bf16)v2, (__bf16)v3};
-            } else {
-                *reinterpret_cast<float4 *>(dst) = float4{v0, v1, v2, v3};
-            }
-        }
-    }
+__host__ __device__ __forceinline__ int zchan(int ct, int i) {
+    return 32 * (ct >> 1) + 8 * (i >> 2) + 4 * (ct & 1) + (i & 3);
 }
-
-}  // namespace ts3
-
-namespace ts3 {
 
 // Softmax over one head's M slices for the wave's points, logits laid out
 // [slices x points] (lane (g, p) holds slices 16*mt + 4*g + r of point p):
@@ -215,102 +90,246 @@ __device__ __forceinline__ void softmax_shifted(f32x4 (&L)[MT][PT], Frag<T> (&wf
     }
 }
 
-// Pass 2 with the prepared W2' fragments of every head and the scaled bias
-// resident in LDS (H*M*C storage elements + H*M floats; 130 KB for C=128,
-// H*M=512 in bf16), and each head's Z fragments (16 KB) staged into LDS with
-// direct global->LDS loads shared by the workgroup's four waves.  Persistent
-// workgroups stride over 256-point blocks (64 per wave, 1 wave per SIMD).
-// Per head h: [barrier; stage Z_h] [logits_h] [softmax_h] [barrier]
-// [deslice_h].  Every wave runs every block and barrier (tail points are
-// masked), so barriers never diverge.
-template <typename T, int C, int M> struct Pass2LdsCfg {
-    using Base = Pass2Cfg<T, C, M>;
-    static constexpr int ZFRAGS = Base::CT * Base::KM;            // 1 KB fragments per head
-    static constexpr int Z_STAGE_ELEMS = ZFRAGS * 64 * 8;
-    static_assert(ZFRAGS % 4 == 0, "Z fragments split evenly over four waves");
+// out rows of one wave block plus b3: lane (g, li) writes channels
+// 32k + 8g .. +7 of point p0 + 16*pt + li from tiles 2k and 2k+1.
+template <typename T, int CT, int PT, int C>
+__device__ __forceinline__ void store_rows(const f32x4 (&O)[CT][PT], const float *__restrict__ b3,
+                                           T *__restrict__ out, int64_t p0, int64_t n, int g, int li) {
+#pragma unroll
+    for (int k = 0; k < CT / 2; ++k) {
+        const float4 ba = *reinterpret_cast<const float4 *>(b3 + 32 * k + 8 * g);
+        const float4 bb = *reinterpret_cast<const float4 *>(b3 + 32 * k + 8 * g + 4);
+#pragma unroll
+        for (int pt = 0; pt < PT; ++pt) {
+            const int64_t p = p0 + pt * 16 + li;
+            if (p >= n) continue;
+            const f32x4 &u = O[2 * k][pt], &v = O[2 * k + 1][pt];
+            T *dst = out + (size_t)p * C + 32 * k + 8 * g;
+            if constexpr (sizeof(T) == 2) {
+                *reinterpret_cast<bf16x8 *>(dst) =
+                    bf16x8{(__bf16)(u[0] + ba.x), (__bf16)(u[1] + ba.y), (__bf16)(u[2] + ba.z), (__bf16)(u[3] + ba.w),
+                           (__bf16)(v[0] + bb.x), (__bf16)(v[1] + bb.y), (__bf16)(v[2] + bb.z), (__bf16)(v[3] + bb.w)};
+            } else {
+                reinterpret_cast<float4 *>(dst)[0] = float4{u[0] + ba.x, u[1] + ba.y, u[2] + ba.z, u[3] + ba.w};
+                reinterpret_cast<float4 *>(dst)[1] = float4{v[0] + bb.x, v[1] + bb.y, v[2] + bb.z, v[3] + bb.w};
+            }
+        }
+    }
+}
+
+// One wave block decoded from global-memory fragments with the max-shifted
+// softmax: the generic kernel's body, and the rare fallback of the staged one.
+template <typename T, int C, int M, int PT>
+__device__ void deslice_block_global(const T *__restrict__ x, int64_t n, int64_t p0, int32_t H,
+                                     const T *__restrict__ w2p, const float *__restrict__ b2s,
+                                     const T *__restrict__ zp, const float *__restrict__ b3,
+                                     T *__restrict__ out, int lane) {
+    constexpr int CT = C / 16, MT = M / 16, CK = C / 32, KM = M >= 32 ? M / 32 : 1;
+    const int li = lane & 15, g = lane >> 4;
+    // B operand x^T: lane (g, li) holds x[p0 + 16*pt + li][32*kc + 8*g .. +8].
+    Frag<T> xb[PT][CK];
+#pragma unroll
+    for (int pt = 0; pt < PT; ++pt) {
+        const int64_t p = p0 + pt * 16 + li;
+#pragma unroll
+        for (int kc = 0; kc < CK; ++kc) {
+            if (p < n)
+                load8(xb[pt][kc], x + (size_t)p * C + kc * 32 + g * 8);
+            else
+                zero8(xb[pt][kc]);
+        }
+    }
+    f32x4 O[CT][PT];
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+        for (int pt = 0; pt < PT; ++pt) O[ct][pt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    for (int h = 0; h < H; ++h) {
+        f32x4 L[MT][PT];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            const float4 bb = *reinterpret_cast<const float4 *>(b2s + h * M + mt * 16 + g * 4);
+#pragma unroll
+            for (int pt = 0; pt < PT; ++pt) L[mt][pt] = f32x4{bb.x, bb.y, bb.z, bb.w};
+#pragma unroll
+            for (int kc = 0; kc < CK; ++kc) {
+                Frag<T> a;
+                load8(a, w2p + ((((size_t)h * MT + mt) * CK + kc) * 64 + lane) * 8);
+#pragma unroll
+                for (int pt = 0; pt < PT; ++pt) mma(L[mt][pt], a, xb[pt][kc]);
+            }
+        }
+        Frag<T> wf[PT][KM];
+        softmax_shifted<T, MT, PT, KM>(L, wf);
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+            for (int km = 0; km < KM; ++km) {
+                Frag<T> a;
+                load8(a, zp + ((((size_t)h * CT + ct) * KM + km) * 64 + lane) * 8);
+#pragma unroll
+                for (int pt = 0; pt < PT; ++pt) mma(O[ct][pt], a, wf[pt][km]);
+            }
+    }
+    store_rows<T, CT, PT, C>(O, b3, out, p0, n, g, li);
+}
+
+template <typename T, int C, int M> struct Pass2Cfg {
+    static constexpr int PT = sizeof(T) == 2 ? 4 : 2;  // 16-point tiles per wave block
+    static constexpr int WAVES = 4;
+    static constexpr int POINTS_PER_WG = WAVES * 16 * PT;
+};
+
+// Generic decoding kernel (fp32 storage, and shapes whose weights do not fit
+// the staged kernel's LDS): every fragment comes from global memory.
+// x   : [n][C] storage elements; out: [n][C]
+// w2p : prepared W2' fragments [H][MT][CK][64][8] (also the A = W2'^T layout)
+// b2s : scaled bias [H*M]
+// zp  : prepared Z fragments [H][CT][KM][64][8]
+// b3  : [C] float32
+template <typename T, int C, int M>
+__global__ __launch_bounds__(256, 1) void k_deslice(const T *__restrict__ x, int64_t n, int32_t H,
+                                                    const T *__restrict__ w2p,
+                                                    const float *__restrict__ b2s,
+                                                    const T *__restrict__ zp,
+                                                    const float *__restrict__ b3, T *__restrict__ out) {
+    using Cfg = Pass2Cfg<T, C, M>;
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int64_t p0 = ((int64_t)blockIdx.x * Cfg::WAVES + wave) * (16 * Cfg::PT);
+    if (p0 >= n) return;
+    deslice_block_global<T, C, M, Cfg::PT>(x, n, p0, H, w2p, b2s, zp, b3, out, lane);
+}
+
+// Staged decoding kernel for 16-bit storage: eight waves (two per SIMD, so one
+// wave's vector-ALU work issues while the other waits) of 32 points each.
+// LDS holds every head's W2' fragments (H*M*C elements, 128 KB for C=128,
+// H*M=512) and two Z stages of one head each; head h+1's Z is copied by the
+// workgroup (direct global->LDS) while head h is decoded, so each head costs
+// one barrier.  The bias b2' of head h+1 is loaded into registers during head h.
+// Persistent workgroups stride over 256-point blocks; every wave runs every
+// block and barrier (tail points are masked), so barriers never diverge.
+template <typename T, int C, int M> struct Pass2W8Cfg {
+    static constexpr int CT = C / 16, MT = M / 16, CK = C / 32, KM = M >= 32 ? M / 32 : 1;
+    static constexpr int WAVES = 8;
+    static constexpr int PT = 2;
+    static constexpr int POINTS_PER_WG = WAVES * 16 * PT;
+    static constexpr int ZFRAGS = CT * KM;           // 1 KB fragments per head
+    static constexpr int STAGE_ELEMS = ZFRAGS * 512;
+    static constexpr int NSTORE = (CT / 2) * PT;     // output stores per full wave block
+    static constexpr int NXLOAD = PT * CK;           // x loads per wave block
     static size_t lds_bytes(int H) {
-        return (size_t)H * Base::MT * Base::CK * 512 * sizeof(T) + (size_t)H * M * 4 +
-               (size_t)Z_STAGE_ELEMS * sizeof(T);
+        return ((size_t)H * MT * CK * 512 + 2 * (size_t)STAGE_ELEMS) * sizeof(T);
     }
 };
 
 template <typename T, int C, int M>
-__global__ __launch_bounds__(256, 1) void k_deslice_lds(const T *__restrict__ x, int64_t n, int32_t H,
-                                                        const T *__restrict__ w2p,
-                                                        const float *__restrict__ b2s,
-                                                        const T *__restrict__ zp,
-                                                        const float *__restrict__ b3, T *__restrict__ out) {
-    using Cfg = Pass2Cfg<T, C, M>;
-    using LCfg = Pass2LdsCfg<T, C, M>;
+__global__ __launch_bounds__(512, 1) void k_deslice_w8(const T *__restrict__ x, int64_t n, int32_t H,
+                                                       const T *__restrict__ w2p,
+                                                       const float *__restrict__ b2s,
+                                                       const T *__restrict__ zp,
+                                                       const float *__restrict__ b3, T *__restrict__ out) {
+    static_assert(sizeof(T) == 2, "the staged decoder is written for 16-bit storage");
+    using Cfg = Pass2W8Cfg<T, C, M>;
     constexpr int CT = Cfg::CT, MT = Cfg::MT, CK = Cfg::CK, KM = Cfg::KM, PT = Cfg::PT;
-    constexpr int ZFRAGS = LCfg::ZFRAGS;
-    extern __shared__ __attribute__((aligned(16))) unsigned char lds_raw[];
-    T *w2l = reinterpret_cast<T *>(lds_raw);
-    const int64_t w2_elems = (int64_t)H * MT * CK * 64 * 8;
-    float *b2l = reinterpret_cast<float *>(w2l + w2_elems);
-    T *zl = reinterpret_cast<T *>(b2l + H * M);
+    constexpr int ZFRAGS = Cfg::ZFRAGS, WAVES = Cfg::WAVES;
+    extern __shared__ __attribute__((aligned(1024))) unsigned char lds_raw[];
+    T *const w2l = reinterpret_cast<T *>(lds_raw);
+    T *const zs = w2l + (size_t)H * MT * CK * 512;  // two stages of STAGE_ELEMS
     const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     const int li = lane & 15;
     const int g = lane >> 4;
+    const int64_t nblk = (n + Cfg::POINTS_PER_WG - 1) / Cfg::POINTS_PER_WG;
+    if (n <= 0) return;
 
-    {   // stage every head's W2' fragments and the scaled bias once
-        const int64_t total16 = w2_elems * (int64_t)sizeof(T) / 16;
+    {   // every head's W2' fragments, once (read after the first head's barrier)
+        const int64_t total16 = (int64_t)H * MT * CK * 512 * (int64_t)sizeof(T) / 16;
         const uint4 *src = reinterpret_cast<const uint4 *>(w2p);
         uint4 *dst = reinterpret_cast<uint4 *>(w2l);
-        for (int64_t i = threadIdx.x; i < total16; i += 256) dst[i] = src[i];
-        for (int i = threadIdx.x; i < H * M; i += 256) b2l[i] = b2s[i];
+        for (int64_t i = threadIdx.x; i < total16; i += WAVES * 64) dst[i] = src[i];
     }
-    __syncthreads();
 
-    // Wave w copies Z fragments w, w+4, ... of head h into the stage (1 KB each).
-    auto stage_z = [&](int h) {
+    // Head h's Z fragments into stage s: wave w copies fragments w, w+8, ...
+    // (a wave-uniform count of copies).
+    auto stage_z = [&](int h, int s) {
+        T *dst = zs + (size_t)s * Cfg::STAGE_ELEMS;
+        for (int f = wave; f < ZFRAGS; f += WAVES)
+            dma16(zp + ((size_t)h * ZFRAGS + f) * 512 + lane * 8, lds_addr(dst + f * 512));
+    };
+    auto load_bias = [&](int h, f32x4 (&b)[MT]) {
 #pragma unroll
-        for (int i = 0; i < ZFRAGS / 4; ++i) {
-            const int f = wave + 4 * i;
-            __builtin_amdgcn_global_load_lds(
-                (const void *)(zp + ((size_t)h * ZFRAGS + f) * 512 + lane * 8),
-                (__attribute__((address_space(3))) void *)(zl + f * 512), 16, 0, 0);
+        for (int mt = 0; mt < MT; ++mt) {
+            const float4 v = *reinterpret_cast<const float4 *>(b2s + h * M + mt * 16 + g * 4);
+            b[mt] = f32x4{v.x, v.y, v.z, v.w};
         }
     };
-
-    const int64_t nblk = (n + Cfg::POINTS_PER_WG - 1) / Cfg::POINTS_PER_WG;
-
-    // B operand x^T of one block: lane (g, li) holds x[p0 + 16*pt + li][32*kc + 8*g .. +8].
+    // B operand x^T of block blk: lane (g, li) holds x[p0 + 16*pt + li][32*kc +
+    // 8*g .. +8].  Always exactly NXLOAD loads (rows past the end read the last
+    // row and are zeroed), so the wait counts below stay exact.
     auto load_x = [&](int64_t blk, Frag<T> (&xb)[PT][CK]) {
-        const int64_t p0 = (blk * Cfg::WAVES + wave) * (16 * PT);
+        const int64_t p0 = blk * Cfg::POINTS_PER_WG + wave * (16 * PT);
 #pragma unroll
         for (int pt = 0; pt < PT; ++pt) {
             const int64_t p = p0 + pt * 16 + li;
+            const int64_t pc = p < n ? p : n - 1;
 #pragma unroll
-            for (int kc = 0; kc < CK; ++kc) {
-                if (blk < nblk && p < n)
-                    load8(xb[pt][kc], x + (size_t)p * C + kc * 32 + g * 8);
-                else
-                    zero8(xb[pt][kc]);
-            }
+            for (int kc = 0; kc < CK; ++kc) load8(xb[pt][kc], x + (size_t)pc * C + kc * 32 + g * 8);
+            if (p >= n)
+#pragma unroll
+                for (int kc = 0; kc < CK; ++kc) zero8(xb[pt][kc]);
         }
     };
 
-    // x of the next block is loaded during the current block's last head, so
-    // its latency (and the whole device's burst of block loads) overlaps compute.
-    Frag<T> xb[PT][CK], xnext[PT][CK];
-    load_x(blockIdx.x, xnext);
+    // This wave's memory operations in issue order within a block:
+    //   head h (after its barrier): copies of Z_{h+1} and the bias of head h+1
+    //     (for the last head: head 0 of the next block, if there is one);
+    //   last head, once its logits are done: x of the next block (NXLOAD loads,
+    //     into the registers of the current block's x);
+    //   after the last head: NSTORE output stores (full blocks).
+    // Head h's wait lets exactly the operations younger than head h's copies
+    // and bias stay in flight.
+    Frag<T> xb[PT][CK];
+    f32x4 bias[MT];
+    int stage = 0;
+    if ((int64_t)blockIdx.x < nblk) {
+        load_x(blockIdx.x, xb);
+        load_bias(0, bias);
+        stage_z(0, 0);
+    }
+    wait_vmcnt<0>();
+    bool pending = false;  // the previous block left NXLOAD loads + NSTORE stores in flight
     for (int64_t blk = blockIdx.x; blk < nblk; blk += gridDim.x) {
-        const int64_t p0 = (blk * Cfg::WAVES + wave) * (16 * PT);
-#pragma unroll
-        for (int pt = 0; pt < PT; ++pt)
-#pragma unroll
-            for (int kc = 0; kc < CK; ++kc) xb[pt][kc] = xnext[pt][kc];
-
+        const int64_t p0 = blk * Cfg::POINTS_PER_WG + wave * (16 * PT);
+        const bool has_next = blk + gridDim.x < nblk;
         f32x4 O[CT][PT];
-
-        auto logits = [&](int h, f32x4 (&L)[MT][PT]) {
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
-                const float4 bb = *reinterpret_cast<const float4 *>(b2l + h * M + mt * 16 + g * 4);
+        for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
-                for (int pt = 0; pt < PT; ++pt) L[mt][pt] = f32x4{bb.x, bb.y, bb.z, bb.w};
+            for (int pt = 0; pt < PT; ++pt) O[ct][pt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        bool ok = true;
+        for (int h = 0; h < H; ++h) {
+            if (h == 0 && pending) wait_vmcnt<Cfg::NXLOAD + Cfg::NSTORE>();
+            else wait_vmcnt<0>();
+            __syncthreads();  // every copy of Z_h landed; stage s^1 is no longer read
+            f32x4 L[MT][PT];
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int pt = 0; pt < PT; ++pt) L[mt][pt] = bias[mt];
+            const int cur = stage;
+            if (h + 1 < H) {
+                stage_z(h + 1, stage ^ 1);
+                load_bias(h + 1, bias);
+                stage ^= 1;
+            } else if (has_next) {
+                stage_z(0, stage ^ 1);
+                load_bias(0, bias);
+                stage ^= 1;
+            }
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
                 for (int kc = 0; kc < CK; ++kc) {
                     Frag<T> a;
@@ -318,10 +337,10 @@ __global__ __launch_bounds__(256, 1) void k_deslice_lds(const T *__restrict__ x,
 #pragma unroll
                     for (int pt = 0; pt < PT; ++pt) mma(L[mt][pt], a, xb[pt][kc]);
                 }
-            }
-        };
-        // out += Z_h^T . w_h with Z_h in the LDS stage.
-        auto deslice_head = [&](const Frag<T> (&wf)[PT][KM]) {
+            if (h + 1 == H && has_next) load_x(blk + gridDim.x, xb);
+            Frag<T> wf[PT][KM];
+            ok = softmax_unshifted<T, MT, PT, KM>(L, wf) && ok;
+            const T *zl = zs + (size_t)cur * Cfg::STAGE_ELEMS;
 #pragma unroll
             for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
@@ -331,64 +350,23 @@ __global__ __launch_bounds__(256, 1) void k_deslice_lds(const T *__restrict__ x,
 #pragma unroll
                     for (int pt = 0; pt < PT; ++pt) mma(O[ct][pt], a, wf[pt][km]);
                 }
-        };
-
-        // All heads of the block.  Per head: [barrier; stage Z_h] [logits_h]
-        // [softmax_h] [wait; barrier] [deslice_h].  SHIFTED selects the
-        // max-shifted softmax; the unshifted pass reports whether every row of
-        // this wave was in the safe window.  PREFETCH loads the next block's x
-        // once the last head's logits no longer need this block's.
-        auto run_heads = [&](auto shifted, bool prefetch) -> bool {
-#pragma unroll
-            for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-                for (int pt = 0; pt < PT; ++pt) O[ct][pt] = f32x4{0.f, 0.f, 0.f, 0.f};
-            bool ok = true;
-            for (int hh = 0; hh < H; ++hh) {
-                __syncthreads();  // every wave is done reading the stage
-                stage_z(hh);
-                f32x4 L[MT][PT];
-                logits(hh, L);
-                if (prefetch && hh == H - 1) load_x(blk + gridDim.x, xnext);
-                Frag<T> wf[PT][KM];
-                if constexpr (decltype(shifted)::value)
-                    softmax_shifted<T, MT, PT, KM>(L, wf);
-                else
-                    ok = softmax_unshifted<T, MT, PT, KM>(L, wf) && ok;
-                __builtin_amdgcn_s_waitcnt(0);  // this wave's stage loads have landed
-                __syncthreads();                // ... and every other wave's
-                deslice_head(wf);
-            }
-            return ok;
-        };
-        // Workgroup-uniform fallback: if any wave saw a row outside the safe
-        // window, all waves redo the block with the max-shifted softmax.
-        const bool ok = run_heads(std::false_type{}, true);
-        if (__syncthreads_or(!ok)) {
-            load_x(blk, xb);
-            run_heads(std::true_type{}, false);
-            load_x(blk + gridDim.x, xnext);
         }
-
-#pragma unroll
-        for (int ct = 0; ct < CT; ++ct) {
-            const float4 bb = *reinterpret_cast<const float4 *>(b3 + ct * 16 + g * 4);
-#pragma unroll
-            for (int pt = 0; pt < PT; ++pt) {
-                const int64_t p = p0 + pt * 16 + li;
-                if (p >= n) continue;
-                const float v0 = O[ct][pt][0] + bb.x, v1 = O[ct][pt][1] + bb.y;
-                const float v2 = O[ct][pt][2] + bb.z, v3 = O[ct][pt][3] + bb.w;
-                T *dst = out + (size_t)p * C + ct * 16 + g * 4;
-                if constexpr (sizeof(T) == 2) {
-                    typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
-                    *reinterpret_cast<bf16x4 *>(dst) = bf16x4{(__bf16)v0, (__bf16)v1, (__bf16)v2, (__bf16)v3};
-                } else {
-                    *reinterpret_cast<float4 *>(dst) = float4{v0, v1, v2, v3};
-                }
-            }
+        if (ok) {
+            store_rows<T, CT, PT, C>(O, b3, out, p0, n, g, li);
+        } else {
+            // Rare: a row's exp2 sum left the safe window.  This wave redoes
+            // its block from global-memory fragments with the shifted softmax
+            // (no barriers inside), 16 points at a time.
+            #pragma unroll 1
+            for (int pt = 0; pt < PT; ++pt)  // 16 points at a time keeps its registers small
+                deslice_block_global<T, C, M, 1>(x, n, p0 + 16 * pt, H, w2p, b2s, zp, b3, out, lane);
         }
+        // Only a full block on the fast path with a successor leaves exactly
+        // NXLOAD + NSTORE operations behind its last copies; otherwise drain.
+        pending = ok && has_next && p0 + 16 * PT <= n;
+        if (!pending) wait_vmcnt<0>();
     }
+    wait_vmcnt<0>();
 }
 
 }  // namespace ts3

@@ -36,7 +36,7 @@ __global__ void k_prep_w2(const float *__restrict__ W2, const float *__restrict_
 }
 
 // Z in decoding-operand order [H][CT][KM][64][8]: lane l, slot t holds
-// Z[h][32*km + 16*(t>>2) + 4*(l>>4) + (t&3)][16*ct + (l&15)] (zero past M).
+// Z[h][32*km + 16*(t>>2) + 4*(l>>4) + (t&3)][zchan(ct, l&15)] (zero past M).
 template <typename T>
 __global__ void k_prep_z(const float *__restrict__ Z, int C, int H, int M, T *__restrict__ zp) {
     const int CT = C / 16, KM = M >= 32 ? M / 32 : 1;
@@ -49,7 +49,7 @@ __global__ void k_prep_z(const float *__restrict__ Z, int C, int H, int M, T *__
         const int ct = (int)(r % CT);
         const int h = (int)(r / CT);
         const int m = km * 32 + (t >> 2) * 16 + (lane >> 4) * 4 + (t & 3);
-        const int c = ct * 16 + (lane & 15);
+        const int c = zchan(ct, lane & 15);
         store_elem(zp + i, m < M ? Z[((int64_t)h * M + m) * C + c] : 0.f);
     }
 }
