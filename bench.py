@@ -102,13 +102,13 @@ def summarize_traffic(fetch_dir: str, write_dir: str, command: str):
         factor = CAL_BYTES / (float(cal["Counter_Value"]) * 1024.0)
         out.setdefault("calibration", {})[name] = {"copy_bytes": CAL_BYTES, "counter_kib": float(cal["Counter_Value"]),
                                                   "bytes_per_counted_byte": factor}
-        for kname in ("k_slice_accumulate", "k_deslice_lds"):
+        for kname in ("k_slice_accumulate", "k_deslice_w8"):
             vals = [float(r["Counter_Value"]) for r in rs if kname + "<" in r["Kernel_Name"]]
             per.setdefault(kname, {})[name] = (sum(vals) / len(vals), len(vals), factor)
     for kname, d in per.items():
         f_kib, n, f_fac = d["FETCH_SIZE"]
         w_kib, _, w_fac = d["WRITE_SIZE"]
-        out["kernels"]["k_deslice" if kname == "k_deslice_lds" else kname] = {
+        out["kernels"][kname] = {
             "points": 1_000_000, "dispatches": n, "fetch_kib": f_kib, "write_kib": w_kib,
             "hbm_bytes_per_launch": f_kib * 1024 * f_fac + w_kib * 1024 * w_fac}
     path = os.path.join(ROOT, "profiles", "traffic.json")
@@ -226,7 +226,7 @@ def main():
     if t_p1 >= t_p2:
         kname, t_launch, nl = "k_slice_accumulate", t_p1 / ntile, ntile
     else:
-        kname, t_launch, nl = "k_deslice", t_p2 / nchunk, nchunk
+        kname, t_launch, nl = "k_deslice_w8", t_p2 / nchunk, nchunk
     pts_launch = min(wl.tile, N)
     achieved = flop_per_point * pts_launch / (t_launch * 1e-3) / 1e12
     traffic = measured_traffic(kname, pts_launch)
