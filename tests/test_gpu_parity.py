@@ -163,6 +163,42 @@ def test_one_hot_slices_fp32():
     assert normwise(got, ref) <= FP32_TOL
 
 
+def test_bf16_shifted_softmax_fallback_mixed_with_fast_path():
+    """bf16 at the benchmark shape with a region of points whose logits overflow
+    exp2 (sums outside [2^-100, 2^100]): the blocks holding them take the
+    max-shifted path in both passes, the others the unshifted one."""
+    C, H, M, N = 128, 8, 64, 6000
+    banner("bf16 softmax fallback mixed with the fast path")
+    from ts3_synth import round_bf16
+    rng = np.random.default_rng(21)
+    W = make_weights(C, H, M, C // H, seed=5, bias_seed=6)
+    W2 = W["W2"].astype(np.float64)
+    it = 2.0
+    x = rng.standard_normal((N, C))
+    # points lo..hi-1 point along one W2 column per head, scaled so that each
+    # head's largest logit exceeds 2^130 in exp2 units (the unshifted sum
+    # overflows); candidates whose weights are not one-hot by a wide margin
+    # (top two logits under 24 exp2 units apart) are dropped
+    lo, hi = 2100, 2900
+    cols = rng.integers(0, M, size=(2000, H)) + np.arange(H) * M
+    cand = round_bf16(300.0 * W2[:, cols].sum(axis=2).T + 0.1 * rng.standard_normal((2000, C)))
+    lgc = np.sort((cand @ W2).reshape(-1, H, M), axis=2) * it / np.log(2.0)
+    good = ((lgc[:, :, -1] - lgc[:, :, -2]).min(axis=1) > 24) & (lgc[:, :, -1].max(axis=1) > 130)
+    assert good.sum() >= hi - lo
+    x[lo:hi] = cand[good][:hi - lo]
+    x = round_bf16(x)
+    lg = (x @ W2) * it / np.log(2.0)
+    assert np.abs(lg[:lo]).max() < 40 and np.abs(lg[hi:]).max() < 40   # fast-path rows elsewhere
+    got, st, _ = _run(x, W, C, H, M, "bf16", 1 / it, 1536, 1000, 512)
+    ref = oracle.layer_forward_fast(x, W, H, M, it)
+    ref_st = oracle.build_state(x, W, H, M, it)
+    e_out, e_z = rel_l2(got, ref), rel_l2(st["Z"], ref_st["Z"])
+    print(f"rel L2 out {e_out:.3e}  Z {e_z:.3e}")
+    assert e_out <= BF16_TOL and e_z <= BF16_TOL
+    for k in ("s_raw", "d"):
+        assert rel_l2(st[k], ref_st[k]) <= BF16_TOL, k
+
+
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
 def test_permuted_and_duplicated_points(dtype):
     torch = _torch()
