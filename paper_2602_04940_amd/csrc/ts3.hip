@@ -56,8 +56,8 @@ enum Phase { PH_RESET = 0, PH_ACCUM = 1, PH_FINAL = 2, PH_ATTEND = 3 };
 struct Kernels {
     void (*pass1)(const void *, int64_t, int64_t, int32_t, int32_t, int32_t, const void *, const float *,
                   float *, hipStream_t);
-    hipError_t (*pass2)(const void *, int64_t, int32_t, const void *, const float *, const void *,
-                        const float *, void *, hipStream_t);
+    hipError_t (*pass2)(const void *, int64_t, int32_t, const void *, const float *, const void *, void *,
+                        hipStream_t);
 };
 
 template <typename T, int C, int M>
@@ -80,7 +80,7 @@ int device_cu_count() {
 
 template <typename T, int C, int M>
 hipError_t launch_pass2(const void *x, int64_t n, int32_t H, const void *w2p, const float *b2s,
-                        const void *zp, const float *b3, void *out, hipStream_t st) {
+                        const void *zp, void *out, hipStream_t st) {
     using Cfg = Pass2Cfg<T, C, M>;
     const int64_t nblk = (n + Cfg::POINTS_PER_WG - 1) / Cfg::POINTS_PER_WG;
     if constexpr (sizeof(T) == 2) {
@@ -103,13 +103,13 @@ hipError_t launch_pass2(const void *x, int64_t n, int32_t H, const void *w2p, co
             const int64_t wblk = (n + WCfg::POINTS_PER_WG - 1) / WCfg::POINTS_PER_WG;
             const int64_t grid = std::min<int64_t>(wblk, device_cu_count());
             hipLaunchKernelGGL((k_deslice_w8<T, C, M>), dim3((unsigned)grid), dim3(64 * WCfg::WAVES), lds, st,
-                               (const T *)x, n, H, (const T *)w2p, b2s, (const T *)zp, b3, (T *)out);
+                               (const T *)x, n, H, (const T *)w2p, b2s, (const T *)zp, (T *)out);
             return hipSuccess;
         }
     }
     {
         hipLaunchKernelGGL((k_deslice<T, C, M>), dim3((unsigned)nblk), dim3(256), 0, st, (const T *)x, n, H,
-                           (const T *)w2p, b2s, (const T *)zp, b3, (T *)out);
+                           (const T *)w2p, b2s, (const T *)zp, (T *)out);
     }
     return hipSuccess;
 }
@@ -216,10 +216,10 @@ ts3_status prep_z(ts3_state *st, hipStream_t stream) {
     const int64_t total = (int64_t)d.H * (d.C / 16) * KM * 512;
     const int grid = (int)std::min<int64_t>((total + 255) / 256, 4096);
     if (d.io_dtype == TS3_BF16)
-        hipLaunchKernelGGL(k_prep_z<bf16_t>, dim3(grid), dim3(256), 0, stream, st->Z, d.C, d.H, d.M,
+        hipLaunchKernelGGL(k_prep_z<bf16_t>, dim3(grid), dim3(256), 0, stream, st->Z, st->b3, d.C, d.H, d.M,
                            (bf16_t *)st->zp);
     else
-        hipLaunchKernelGGL(k_prep_z<float>, dim3(grid), dim3(256), 0, stream, st->Z, d.C, d.H, d.M,
+        hipLaunchKernelGGL(k_prep_z<float>, dim3(grid), dim3(256), 0, stream, st->Z, st->b3, d.C, d.H, d.M,
                            (float *)st->zp);
     LAUNCH_CHECK("prep_z");
     return TS3_OK;
@@ -416,13 +416,13 @@ ts3_status ts3_token_attention(ts3_state *st, const ts3_weights *w, void *stream
     hipLaunchKernelGGL(k_attention, dim3(d.H), dim3(256), lds, hs, st->s, w->Wq, w->Wk, w->Wv, w->W3, d.C, d.H,
                        d.M, d.dh, st->s1, st->Z);
     LAUNCH_CHECK("attention");
-    ts3_status s = prep_z(st, hs);
-    if (s != TS3_OK) return s;
     if (w->b3)
         HIP_TRY(hipMemcpyAsync(st->b3, w->b3, (size_t)d.C * 4, hipMemcpyDeviceToDevice, hs));
     else
         hipLaunchKernelGGL(k_zero, dim3(1), dim3(256), 0, hs, st->b3, (int64_t)d.C);
     LAUNCH_CHECK("b3");
+    ts3_status s = prep_z(st, hs);  // folds b3 into the prepared Z
+    if (s != TS3_OK) return s;
     st->phase = PH_ATTEND;
     return TS3_OK;
 }
@@ -442,7 +442,7 @@ ts3_status ts3_deslice(const ts3_state *st, const ts3_weights *w, const void *x_
     const ts3_desc &d = st->desc;
     if (n_chunk > ((int64_t)INT32_MAX) * 64) return fail(TS3_ERR_INVALID_ARG, "n_chunk too large for one launch");
     const hipError_t le =
-        st->k.pass2(x_chunk, n_chunk, d.H, st->w2p, st->b2s, st->zp, st->b3, out_chunk, (hipStream_t)stream);
+        st->k.pass2(x_chunk, n_chunk, d.H, st->w2p, st->b2s, st->zp, out_chunk, (hipStream_t)stream);
     if (le != hipSuccess) return fail(TS3_ERR_HIP, "deslice LDS setup: %s", hipGetErrorString(le));
     LAUNCH_CHECK("deslice");
     return TS3_OK;

@@ -90,15 +90,13 @@ __device__ __forceinline__ void softmax_shifted(f32x4 (&L)[MT][PT], Frag<T> (&wf
     }
 }
 
-// out rows of one wave block plus b3: lane (g, li) writes channels
-// 32k + 8g .. +7 of point p0 + 16*pt + li from tiles 2k and 2k+1.
+// out rows of one wave block (b3 is folded into the prepared Z): lane (g, li)
+// writes channels 32k + 8g .. +7 of point p0 + 16*pt + li from tiles 2k and 2k+1.
 template <typename T, int CT, int PT, int C>
-__device__ __forceinline__ void store_rows(const f32x4 (&O)[CT][PT], const float *__restrict__ b3,
-                                           T *__restrict__ out, int64_t p0, int64_t n, int g, int li) {
+__device__ __forceinline__ void store_rows(const f32x4 (&O)[CT][PT], T *__restrict__ out, int64_t p0, int64_t n,
+                                           int g, int li) {
 #pragma unroll
     for (int k = 0; k < CT / 2; ++k) {
-        const float4 ba = *reinterpret_cast<const float4 *>(b3 + 32 * k + 8 * g);
-        const float4 bb = *reinterpret_cast<const float4 *>(b3 + 32 * k + 8 * g + 4);
 #pragma unroll
         for (int pt = 0; pt < PT; ++pt) {
             const int64_t p = p0 + pt * 16 + li;
@@ -106,12 +104,11 @@ __device__ __forceinline__ void store_rows(const f32x4 (&O)[CT][PT], const float
             const f32x4 &u = O[2 * k][pt], &v = O[2 * k + 1][pt];
             T *dst = out + (size_t)p * C + 32 * k + 8 * g;
             if constexpr (sizeof(T) == 2) {
-                *reinterpret_cast<bf16x8 *>(dst) =
-                    bf16x8{(__bf16)(u[0] + ba.x), (__bf16)(u[1] + ba.y), (__bf16)(u[2] + ba.z), (__bf16)(u[3] + ba.w),
-                           (__bf16)(v[0] + bb.x), (__bf16)(v[1] + bb.y), (__bf16)(v[2] + bb.z), (__bf16)(v[3] + bb.w)};
+                *reinterpret_cast<bf16x8 *>(dst) = bf16x8{(__bf16)u[0], (__bf16)u[1], (__bf16)u[2], (__bf16)u[3],
+                                                          (__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
             } else {
-                reinterpret_cast<float4 *>(dst)[0] = float4{u[0] + ba.x, u[1] + ba.y, u[2] + ba.z, u[3] + ba.w};
-                reinterpret_cast<float4 *>(dst)[1] = float4{v[0] + bb.x, v[1] + bb.y, v[2] + bb.z, v[3] + bb.w};
+                reinterpret_cast<float4 *>(dst)[0] = float4{u[0], u[1], u[2], u[3]};
+                reinterpret_cast<float4 *>(dst)[1] = float4{v[0], v[1], v[2], v[3]};
             }
         }
     }
@@ -122,8 +119,7 @@ __device__ __forceinline__ void store_rows(const f32x4 (&O)[CT][PT], const float
 template <typename T, int C, int M, int PT>
 __device__ void deslice_block_global(const T *__restrict__ x, int64_t n, int64_t p0, int32_t H,
                                      const T *__restrict__ w2p, const float *__restrict__ b2s,
-                                     const T *__restrict__ zp, const float *__restrict__ b3,
-                                     T *__restrict__ out, int lane) {
+                                     const T *__restrict__ zp, T *__restrict__ out, int lane) {
     constexpr int CT = C / 16, MT = M / 16, CK = C / 32, KM = M >= 32 ? M / 32 : 1;
     const int li = lane & 15, g = lane >> 4;
     // B operand x^T: lane (g, li) holds x[p0 + 16*pt + li][32*kc + 8*g .. +8].
@@ -172,7 +168,7 @@ __device__ void deslice_block_global(const T *__restrict__ x, int64_t n, int64_t
                 for (int pt = 0; pt < PT; ++pt) mma(O[ct][pt], a, wf[pt][km]);
             }
     }
-    store_rows<T, CT, PT, C>(O, b3, out, p0, n, g, li);
+    store_rows<T, CT, PT, C>(O, out, p0, n, g, li);
 }
 
 template <typename T, int C, int M> struct Pass2Cfg {
@@ -186,20 +182,18 @@ template <typename T, int C, int M> struct Pass2Cfg {
 // x   : [n][C] storage elements; out: [n][C]
 // w2p : prepared W2' fragments [H][MT][CK][64][8] (also the A = W2'^T layout)
 // b2s : scaled bias [H*M]
-// zp  : prepared Z fragments [H][CT][KM][64][8]
-// b3  : [C] float32
+// zp  : prepared Z fragments [H][CT][KM][64][8], b3/H folded in
 template <typename T, int C, int M>
 __global__ __launch_bounds__(256, 1) void k_deslice(const T *__restrict__ x, int64_t n, int32_t H,
                                                     const T *__restrict__ w2p,
                                                     const float *__restrict__ b2s,
-                                                    const T *__restrict__ zp,
-                                                    const float *__restrict__ b3, T *__restrict__ out) {
+                                                    const T *__restrict__ zp, T *__restrict__ out) {
     using Cfg = Pass2Cfg<T, C, M>;
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int64_t p0 = ((int64_t)blockIdx.x * Cfg::WAVES + wave) * (16 * Cfg::PT);
     if (p0 >= n) return;
-    deslice_block_global<T, C, M, Cfg::PT>(x, n, p0, H, w2p, b2s, zp, b3, out, lane);
+    deslice_block_global<T, C, M, Cfg::PT>(x, n, p0, H, w2p, b2s, zp, out, lane);
 }
 
 // Staged decoding kernel for 16-bit storage: eight waves (two per SIMD, so one
@@ -228,8 +222,7 @@ template <typename T, int C, int M>
 __global__ __launch_bounds__(512, 1) void k_deslice_w8(const T *__restrict__ x, int64_t n, int32_t H,
                                                        const T *__restrict__ w2p,
                                                        const float *__restrict__ b2s,
-                                                       const T *__restrict__ zp,
-                                                       const float *__restrict__ b3, T *__restrict__ out) {
+                                                       const T *__restrict__ zp, T *__restrict__ out) {
     static_assert(sizeof(T) == 2, "the staged decoder is written for 16-bit storage");
     using Cfg = Pass2W8Cfg<T, C, M>;
     constexpr int CT = Cfg::CT, MT = Cfg::MT, CK = Cfg::CK, KM = Cfg::KM, PT = Cfg::PT;
@@ -328,10 +321,12 @@ __global__ __launch_bounds__(512, 1) void k_deslice_w8(const T *__restrict__ x, 
                 load_bias(0, bias);
                 stage ^= 1;
             }
+            // K steps outermost: consecutive MFMAs go to the 2*MT independent
+            // accumulators instead of chaining on one.
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
+            for (int kc = 0; kc < CK; ++kc)
 #pragma unroll
-                for (int kc = 0; kc < CK; ++kc) {
+                for (int mt = 0; mt < MT; ++mt) {
                     Frag<T> a;
                     load8(a, w2l + ((((size_t)h * MT + mt) * CK + kc) * 64 + lane) * 8);
 #pragma unroll
@@ -352,14 +347,14 @@ __global__ __launch_bounds__(512, 1) void k_deslice_w8(const T *__restrict__ x, 
                 }
         }
         if (ok) {
-            store_rows<T, CT, PT, C>(O, b3, out, p0, n, g, li);
+            store_rows<T, CT, PT, C>(O, out, p0, n, g, li);
         } else {
             // Rare: a row's exp2 sum left the safe window.  This wave redoes
             // its block from global-memory fragments with the shifted softmax
             // (no barriers inside), 16 points at a time.
             #pragma unroll 1
             for (int pt = 0; pt < PT; ++pt)  // 16 points at a time keeps its registers small
-                deslice_block_global<T, C, M, 1>(x, n, p0 + 16 * pt, H, w2p, b2s, zp, b3, out, lane);
+                deslice_block_global<T, C, M, 1>(x, n, p0 + 16 * pt, H, w2p, b2s, zp, out, lane);
         }
         // Only a full block on the fast path with a successor leaves exactly
         // NXLOAD + NSTORE operations behind its last copies; otherwise drain.

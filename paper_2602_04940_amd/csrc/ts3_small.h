@@ -36,10 +36,14 @@ __global__ void k_prep_w2(const float *__restrict__ W2, const float *__restrict_
 }
 
 // Z in decoding-operand order [H][CT][KM][64][8]: lane l, slot t holds
-// Z[h][32*km + 16*(t>>2) + 4*(l>>4) + (t&3)][zchan(ct, l&15)] (zero past M).
+// Z[h][32*km + 16*(t>>2) + 4*(l>>4) + (t&3)][zchan(ct, l&15)] + b3[c] / H (zero
+// past M).  Each head's slice weights sum to one (Eq. (1)), so the H heads of
+// the deslice add b3 exactly once per point and pass 2 needs no bias pass.
 template <typename T>
-__global__ void k_prep_z(const float *__restrict__ Z, int C, int H, int M, T *__restrict__ zp) {
+__global__ void k_prep_z(const float *__restrict__ Z, const float *__restrict__ b3, int C, int H, int M,
+                         T *__restrict__ zp) {
     const int CT = C / 16, KM = M >= 32 ? M / 32 : 1;
+    const float bscale = 1.f / (float)H;
     const int64_t total = (int64_t)H * CT * KM * 64 * 8;
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
          i += (int64_t)gridDim.x * blockDim.x) {
@@ -50,7 +54,7 @@ __global__ void k_prep_z(const float *__restrict__ Z, int C, int H, int M, T *__
         const int h = (int)(r / CT);
         const int m = km * 32 + (t >> 2) * 16 + (lane >> 4) * 4 + (t & 3);
         const int c = zchan(ct, lane & 15);
-        store_elem(zp + i, m < M ? Z[((int64_t)h * M + m) * C + c] : 0.f);
+        store_elem(zp + i, m < M ? Z[((int64_t)h * M + m) * C + c] + b3[c] * bscale : 0.f);
     }
 }
 
