@@ -259,8 +259,9 @@ __global__ __launch_bounds__(512, 1) void k_deslice_w8(const T *__restrict__ x, 
         }
     };
     // B operand x^T of block blk: lane (g, li) holds x[p0 + 16*pt + li][32*kc +
-    // 8*g .. +8].  Always exactly NXLOAD loads (rows past the end read the last
-    // row and are zeroed), so the wait counts below stay exact.
+    // 8*g .. +8].  Always exactly NXLOAD loads, so the wait counts below stay
+    // exact: rows past the end read the last row (finite data; a point's
+    // outputs depend only on its own row, and padding rows are never stored).
     auto load_x = [&](int64_t blk, Frag<T> (&xb)[PT][CK]) {
         const int64_t p0 = blk * Cfg::POINTS_PER_WG + wave * (16 * PT);
 #pragma unroll
@@ -269,9 +270,6 @@ __global__ __launch_bounds__(512, 1) void k_deslice_w8(const T *__restrict__ x, 
             const int64_t pc = p < n ? p : n - 1;
 #pragma unroll
             for (int kc = 0; kc < CK; ++kc) load8(xb[pt][kc], x + (size_t)pc * C + kc * 32 + g * 8);
-            if (p >= n)
-#pragma unroll
-                for (int kc = 0; kc < CK; ++kc) zero8(xb[pt][kc]);
         }
     };
 
@@ -312,13 +310,13 @@ __global__ __launch_bounds__(512, 1) void k_deslice_w8(const T *__restrict__ x, 
 #pragma unroll
                 for (int pt = 0; pt < PT; ++pt) L[mt][pt] = bias[mt];
             const int cur = stage;
-            if (h + 1 < H) {
-                stage_z(h + 1, stage ^ 1);
-                load_bias(h + 1, bias);
-                stage ^= 1;
-            } else if (has_next) {
-                stage_z(0, stage ^ 1);
-                load_bias(0, bias);
+            // One code path for both successors (next head, or head 0 of the
+            // next block), so the compiler's wait-count tracking sees a single
+            // issue point for these copies and loads.
+            if (h + 1 < H || has_next) {
+                const int hn = h + 1 < H ? h + 1 : 0;
+                stage_z(hn, stage ^ 1);
+                load_bias(hn, bias);
                 stage ^= 1;
             }
             // K steps outermost: consecutive MFMAs go to the 2*MT independent
