@@ -13,6 +13,7 @@
 
 #include "../../include/ts3.h"
 #include "ts3_pass1.h"
+#include "ts3_pass1w8.h"
 #include "ts3_pass2.h"
 #include "ts3_small.h"
 
@@ -63,8 +64,13 @@ struct Kernels {
 template <typename T, int C, int M>
 void launch_pass1(const void *x, int64_t n, int64_t span0, int32_t Q, int32_t nspan, int32_t H,
                   const void *w2p, const float *b2s, float *partials, hipStream_t st) {
-    hipLaunchKernelGGL((k_slice_accumulate<T, C, M>), dim3(nspan * H), dim3(256), 0, st,
-                       (const T *)x, n, span0, Q, nspan, H, (const T *)w2p, b2s, partials);
+    if constexpr (sizeof(T) == 2 && M >= 32 && C == 128) {
+        hipLaunchKernelGGL((k_slice_accumulate_w8<C, M>), dim3(nspan * H), dim3(512), 0, st,
+                           (const bf16_t *)x, n, span0, Q, nspan, H, (const bf16_t *)w2p, b2s, partials);
+    } else {
+        hipLaunchKernelGGL((k_slice_accumulate<T, C, M>), dim3(nspan * H), dim3(256), 0, st,
+                           (const T *)x, n, span0, Q, nspan, H, (const T *)w2p, b2s, partials);
+    }
 }
 
 int device_cu_count() {

@@ -158,14 +158,14 @@ __device__ __forceinline__ void interleave_mfma_valu() {
 // (starting after MFMA R0); NW LDS writes close the region.
 template <int PRE, int NMFMA, int VPER, int R0, int RPER, int RN, int NW>
 __device__ __forceinline__ void interleave_chain() {
-    __builtin_amdgcn_sched_group_barrier(0x100, PRE, 0);
+    if constexpr (PRE > 0) __builtin_amdgcn_sched_group_barrier(0x100, PRE, 0);
 #pragma unroll
     for (int i = 0; i < NMFMA; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x002, VPER, 0);
         if (i >= R0 && (i - R0) % RPER == 0) __builtin_amdgcn_sched_group_barrier(0x100, RN, 0);
     }
-    __builtin_amdgcn_sched_group_barrier(0x200, NW, 0);
+    if constexpr (NW > 0) __builtin_amdgcn_sched_group_barrier(0x200, NW, 0);
 }
 
 // Direct global->LDS copy of 16 bytes per lane: lane l's bytes land at LDS
