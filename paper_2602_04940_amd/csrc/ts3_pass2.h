@@ -320,29 +320,52 @@ __global__ __launch_bounds__(512, 1) void k_deslice_w8(const T *__restrict__ x, 
                 stage ^= 1;
             }
             // K steps outermost: consecutive MFMAs go to the 2*MT independent
-            // accumulators instead of chaining on one.
+            // accumulators instead of chaining on one; the W2' fragments of
+            // step kc+1 are read while step kc's MFMAs run.
+            {
+                const T *wh = w2l + (size_t)h * MT * CK * 512 + lane * 8;
+                Frag<T> a[2][MT];
 #pragma unroll
-            for (int kc = 0; kc < CK; ++kc)
+                for (int mt = 0; mt < MT; ++mt) load8(a[0][mt], wh + (mt * CK) * 512);
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt) {
-                    Frag<T> a;
-                    load8(a, w2l + ((((size_t)h * MT + mt) * CK + kc) * 64 + lane) * 8);
+                for (int kc = 0; kc < CK; ++kc) {
+                    __builtin_amdgcn_sched_barrier(0);
+                    if (kc + 1 < CK)
 #pragma unroll
-                    for (int pt = 0; pt < PT; ++pt) mma(L[mt][pt], a, xb[pt][kc]);
+                        for (int mt = 0; mt < MT; ++mt) load8(a[(kc + 1) & 1][mt], wh + (mt * CK + kc + 1) * 512);
+#pragma unroll
+                    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                        for (int pt = 0; pt < PT; ++pt) mma(L[mt][pt], a[kc & 1][mt], xb[pt][kc]);
+                    if (kc + 1 < CK) __builtin_amdgcn_sched_group_barrier(0x100, MT, 0);  // next reads first
+                    __builtin_amdgcn_sched_group_barrier(0x008, MT * PT, 0);
                 }
+                __builtin_amdgcn_sched_barrier(0);
+            }
             if (h + 1 == H && has_next) load_x(blk + gridDim.x, xb);
             Frag<T> wf[PT][KM];
             ok = softmax_unshifted<T, MT, PT, KM>(L, wf) && ok;
-            const T *zl = zs + (size_t)cur * Cfg::STAGE_ELEMS;
+            // Z fragments of channel tile ct+1 are read while tile ct's MFMAs run.
+            {
+                const T *zl = zs + (size_t)cur * Cfg::STAGE_ELEMS + lane * 8;
+                Frag<T> a[2][KM];
 #pragma unroll
-            for (int ct = 0; ct < CT; ++ct)
+                for (int km = 0; km < KM; ++km) load8(a[0][km], zl + km * 512);
 #pragma unroll
-                for (int km = 0; km < KM; ++km) {
-                    Frag<T> a;
-                    load8(a, zl + ((ct * KM + km) * 64 + lane) * 8);
+                for (int ct = 0; ct < CT; ++ct) {
+                    __builtin_amdgcn_sched_barrier(0);
+                    if (ct + 1 < CT)
 #pragma unroll
-                    for (int pt = 0; pt < PT; ++pt) mma(O[ct][pt], a, wf[pt][km]);
+                        for (int km = 0; km < KM; ++km) load8(a[(ct + 1) & 1][km], zl + ((ct + 1) * KM + km) * 512);
+#pragma unroll
+                    for (int km = 0; km < KM; ++km)
+#pragma unroll
+                        for (int pt = 0; pt < PT; ++pt) mma(O[ct][pt], a[ct & 1][km], wf[pt][km]);
+                    if (ct + 1 < CT) __builtin_amdgcn_sched_group_barrier(0x100, KM, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x008, KM * PT, 0);
                 }
+                __builtin_amdgcn_sched_barrier(0);
+            }
         }
         if (ok) {
             store_rows<T, CT, PT, C>(O, out, p0, n, g, li);
