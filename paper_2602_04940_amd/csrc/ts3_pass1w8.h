@@ -140,17 +140,24 @@ __global__ __launch_bounds__(512, 1) void k_slice_accumulate_w8(
     uint32_t wt0 = wbase + woff<WROW>(8 * g + (li >> 2), 8 * (li & 3));
     uint32_t ws0 = wbase + woff<WROW>(prow(hf, li), 8 * g);
 
+    // The x fragment of step kc+1 is read while step kc's MFMAs run.
     auto logits = [&](auto slot, f32x4 (&L)[MT]) {
         constexpr int SL = decltype(slot)::value;
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) L[mt] = bias[mt];
+        Frag<T> xb[2];
+        xb[0].v = *reinterpret_cast<const bf16x8 *>(lds + xl0 + SL * XTILE);
 #pragma unroll
         for (int kc = 0; kc < CK; ++kc) {
-            Frag<T> xb;
-            xb.v = *reinterpret_cast<const bf16x8 *>(lds + (xl0 ^ (kc << 6)) + SL * XTILE);
+            __builtin_amdgcn_sched_barrier(0);
+            if (kc + 1 < CK)
+                xb[(kc + 1) & 1].v = *reinterpret_cast<const bf16x8 *>(lds + (xl0 ^ ((kc + 1) << 6)) + SL * XTILE);
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt) mma(L[mt], w2[mt][kc], xb);
+            for (int mt = 0; mt < MT; ++mt) mma(L[mt], w2[mt][kc], xb[kc & 1]);
+            if (kc + 1 < CK) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, MT, 0);
         }
+        __builtin_amdgcn_sched_barrier(0);
     };
     auto read_a = [&](auto slot, Frag<T> (&a)[MTH]) {
         constexpr int SL = decltype(slot)::value;
