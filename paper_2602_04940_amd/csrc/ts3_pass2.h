@@ -274,7 +274,7 @@ __global__ __launch_bounds__(512, 1) void k_deslice_w8(const T *__restrict__ x, 
     };
 
     // This wave's memory operations in issue order within a block:
-    //   head h (after its barrier): copies of Z_{h+1} and the bias of head h+1
+    //   head h (after its logits): copies of Z_{h+1} and the bias of head h+1
     //     (for the last head: head 0 of the next block, if there is one);
     //   last head, once its logits are done: x of the next block (NXLOAD loads,
     //     into the registers of the current block's x);
@@ -310,15 +310,6 @@ __global__ __launch_bounds__(512, 1) void k_deslice_w8(const T *__restrict__ x, 
 #pragma unroll
                 for (int pt = 0; pt < PT; ++pt) L[mt][pt] = bias[mt];
             const int cur = stage;
-            // One code path for both successors (next head, or head 0 of the
-            // next block), so the compiler's wait-count tracking sees a single
-            // issue point for these copies and loads.
-            if (h + 1 < H || has_next) {
-                const int hn = h + 1 < H ? h + 1 : 0;
-                stage_z(hn, stage ^ 1);
-                load_bias(hn, bias);
-                stage ^= 1;
-            }
             // K steps outermost: consecutive MFMAs go to the 2*MT independent
             // accumulators instead of chaining on one; the W2' fragments of
             // step kc+1 are read while step kc's MFMAs run.
@@ -342,7 +333,17 @@ __global__ __launch_bounds__(512, 1) void k_deslice_w8(const T *__restrict__ x, 
                 }
                 __builtin_amdgcn_sched_barrier(0);
             }
-            if (h + 1 == H && has_next) load_x(blk + gridDim.x, xb);
+            // The next head's Z copies and bias (or head 0's of the next
+            // block): issued after the logits rather than at the barrier, where
+            // every wave would queue them at once.  One code path for both
+            // successors, so the compiler's wait counts see one issue point.
+            if (h + 1 < H || has_next) {
+                const int hn = h + 1 < H ? h + 1 : 0;
+                stage_z(hn, stage ^ 1);
+                load_bias(hn, bias);
+                stage ^= 1;
+            }
+            if (h + 1 == H && has_next) load_x(blk + gridDim.x, xb);  // younger than the copies above
             Frag<T> wf[PT][KM];
             ok = softmax_unshifted<T, MT, PT, KM>(L, wf) && ok;
             // Z fragments of channel tile ct+1 are read while tile ct's MFMAs run.
