@@ -106,10 +106,19 @@ hipError_t launch_pass2(const void *x, int64_t n, int32_t H, const void *w2p, co
                     return hipGetLastError();
                 dyn_set = lds;
             }
-            const int64_t wblk = (n + WCfg::POINTS_PER_WG - 1) / WCfg::POINTS_PER_WG;
-            const int64_t grid = std::min<int64_t>(wblk, device_cu_count());
-            hipLaunchKernelGGL((k_deslice_w8<T, C, M>), dim3((unsigned)grid), dim3(64 * WCfg::WAVES), lds, st,
-                               (const T *)x, n, H, (const T *)w2p, b2s, (const T *)zp, (T *)out);
+            // At most P2_MAX_ITERS blocks per workgroup and launch (the kernel
+            // records slow-path blocks in a 64-bit mask); larger calls are
+            // split, which changes no result: every point is decoded alone.
+            const int64_t cus = device_cu_count();
+            const int64_t span = cus * P2_MAX_ITERS * WCfg::POINTS_PER_WG;
+            for (int64_t off = 0; off < n; off += span) {
+                const int64_t m = std::min<int64_t>(span, n - off);
+                const int64_t wblk = (m + WCfg::POINTS_PER_WG - 1) / WCfg::POINTS_PER_WG;
+                const int64_t grid = std::min<int64_t>(wblk, cus);
+                hipLaunchKernelGGL((k_deslice_w8<T, C, M>), dim3((unsigned)grid), dim3(64 * WCfg::WAVES), lds, st,
+                                   (const T *)x + off * C, m, H, (const T *)w2p, b2s, (const T *)zp,
+                                   (T *)out + off * C);
+            }
             return hipSuccess;
         }
     }

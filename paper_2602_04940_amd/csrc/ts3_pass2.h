@@ -201,9 +201,17 @@ __global__ __launch_bounds__(256, 1) void k_deslice(const T *__restrict__ x, int
 // LDS holds every head's W2' fragments (H*M*C elements, 128 KB for C=128,
 // H*M=512) and two Z stages of one head each; head h+1's Z is copied by the
 // workgroup (direct global->LDS) while head h is decoded, so each head costs
-// one barrier.  The bias b2' of head h+1 is loaded into registers during head h.
-// Persistent workgroups stride over 256-point blocks; every wave runs every
-// block and barrier (tail points are masked), so barriers never diverge.
+// one barrier.  The bias b2' of head h+1 is loaded into registers during head
+// h, and the next block's x is loaded during the current block, a fragment or
+// two per head into a second register set, so no block boundary waits on
+// memory.  Persistent workgroups stride over 256-point blocks (at most
+// P2_MAX_ITERS per launch); every wave runs every block and barrier (tail
+// points are masked), so barriers never diverge.  A block whose softmax left
+// the unshifted path's safe window is stored anyway and redone after the main
+// loop (recorded in a wave-uniform bit mask), which keeps the slow path's
+// registers out of the main loop.
+constexpr int P2_MAX_ITERS = 64;
+
 template <typename T, int C, int M> struct Pass2W8Cfg {
     static constexpr int CT = C / 16, MT = M / 16, CK = C / 32, KM = M >= 32 ? M / 32 : 1;
     static constexpr int WAVES = 8;
@@ -226,7 +234,7 @@ __global__ __launch_bounds__(512, 1) void k_deslice_w8(const T *__restrict__ x, 
     static_assert(sizeof(T) == 2, "the staged decoder is written for 16-bit storage");
     using Cfg = Pass2W8Cfg<T, C, M>;
     constexpr int CT = Cfg::CT, MT = Cfg::MT, CK = Cfg::CK, KM = Cfg::KM, PT = Cfg::PT;
-    constexpr int ZFRAGS = Cfg::ZFRAGS, WAVES = Cfg::WAVES;
+    constexpr int ZFRAGS = Cfg::ZFRAGS, WAVES = Cfg::WAVES, NSTORE = Cfg::NSTORE, NXLOAD = Cfg::NXLOAD;
     extern __shared__ __attribute__((aligned(1024))) unsigned char lds_raw[];
     T *const w2l = reinterpret_cast<T *>(lds_raw);
     T *const zs = w2l + (size_t)H * MT * CK * 512;  // two stages of STAGE_ELEMS
@@ -235,13 +243,14 @@ __global__ __launch_bounds__(512, 1) void k_deslice_w8(const T *__restrict__ x, 
     const int li = lane & 15;
     const int g = lane >> 4;
     const int64_t nblk = (n + Cfg::POINTS_PER_WG - 1) / Cfg::POINTS_PER_WG;
-    if (n <= 0) return;
+    if (n <= 0 || H <= 0 || (int64_t)blockIdx.x >= nblk) return;  // uniform over the workgroup
+    const int iters = (int)((nblk - 1 - blockIdx.x) / gridDim.x + 1);  // <= P2_MAX_ITERS (host)
 
-    {   // every head's W2' fragments, once (read after the first head's barrier)
-        const int64_t total16 = (int64_t)H * MT * CK * 512 * (int64_t)sizeof(T) / 16;
-        const uint4 *src = reinterpret_cast<const uint4 *>(w2p);
-        uint4 *dst = reinterpret_cast<uint4 *>(w2l);
-        for (int64_t i = threadIdx.x; i < total16; i += WAVES * 64) dst[i] = src[i];
+    {   // every head's W2' fragments, once: direct copies, all in flight
+        const int64_t total16 = (int64_t)H * MT * CK * 64;  // 16-byte pieces (a multiple of 64)
+        const unsigned char *src = reinterpret_cast<const unsigned char *>(w2p);
+        for (int64_t b = (int64_t)wave * 64; b < total16; b += WAVES * 64)
+            dma16(src + (b + lane) * 16, lds_addr(lds_raw + b * 16));
     }
 
     // Head h's Z fragments into stage s: wave w copies fragments w, w+8, ...
@@ -258,50 +267,51 @@ __global__ __launch_bounds__(512, 1) void k_deslice_w8(const T *__restrict__ x, 
             b[mt] = f32x4{v.x, v.y, v.z, v.w};
         }
     };
-    // B operand x^T of block blk: lane (g, li) holds x[p0 + 16*pt + li][32*kc +
-    // 8*g .. +8].  Always exactly NXLOAD loads, so the wait counts below stay
-    // exact: rows past the end read the last row (finite data; a point's
-    // outputs depend only on its own row, and padding rows are never stored).
-    auto load_x = [&](int64_t blk, Frag<T> (&xb)[PT][CK]) {
-        const int64_t p0 = blk * Cfg::POINTS_PER_WG + wave * (16 * PT);
-#pragma unroll
-        for (int pt = 0; pt < PT; ++pt) {
-            const int64_t p = p0 + pt * 16 + li;
-            const int64_t pc = p < n ? p : n - 1;
-#pragma unroll
-            for (int kc = 0; kc < CK; ++kc) load8(xb[pt][kc], x + (size_t)pc * C + kc * 32 + g * 8);
-        }
+    // Fragment j = (pt, kc) of the B operand x^T of the wave block at p0: lane
+    // (g, li) holds x[p0 + 16*pt + li][32*kc + 8*g .. +8].  Rows past the end
+    // read the last row (finite data; a point's outputs depend only on its own
+    // row, and padding rows are never stored).
+    auto load_xfrag = [&](int64_t p0, int j, Frag<T> (&xf)[PT][CK]) {
+        const int pt = j / CK, kc = j % CK;
+        const int64_t p = p0 + pt * 16 + li;
+        const int64_t pc = p < n ? p : n - 1;
+        load8(xf[pt][kc], x + (size_t)pc * C + kc * 32 + g * 8);
     };
+    // The next block's x fragments are spread over heads 0..H-2 (all at head 0
+    // when H == 1): fragment j goes with head xhead(j).
+    auto xhead = [&](int j) { return H > 1 ? j * (H - 1) / NXLOAD : 0; };
 
-    // This wave's memory operations in issue order within a block:
-    //   head h (after its logits): copies of Z_{h+1} and the bias of head h+1
-    //     (for the last head: head 0 of the next block, if there is one);
-    //   last head, once its logits are done: x of the next block (NXLOAD loads,
-    //     into the registers of the current block's x);
-    //   after the last head: NSTORE output stores (full blocks).
-    // Head h's wait lets exactly the operations younger than head h's copies
-    // and bias stay in flight.
-    Frag<T> xb[PT][CK];
+    const int64_t pw = (int64_t)blockIdx.x * Cfg::POINTS_PER_WG + wave * (16 * PT);
+    const int64_t bstride = (int64_t)gridDim.x * Cfg::POINTS_PER_WG;
+    Frag<T> xA[PT][CK], xB[PT][CK];
     f32x4 bias[MT];
-    int stage = 0;
-    if ((int64_t)blockIdx.x < nblk) {
-        load_x(blockIdx.x, xb);
-        load_bias(0, bias);
-        stage_z(0, 0);
-    }
+#pragma unroll
+    for (int j = 0; j < NXLOAD; ++j) load_xfrag(pw, j, xA);
+    load_bias(0, bias);
+    stage_z(0, 0);
     wait_vmcnt<0>();
-    bool pending = false;  // the previous block left NXLOAD loads + NSTORE stores in flight
-    for (int64_t blk = blockIdx.x; blk < nblk; blk += gridDim.x) {
-        const int64_t p0 = blk * Cfg::POINTS_PER_WG + wave * (16 * PT);
-        const bool has_next = blk + gridDim.x < nblk;
-        f32x4 O[CT][PT];
+    int stage = 0;
+    uint64_t failed = 0;  // bit i: block i left the fast path
+    f32x4 O[CT][PT];
+    // Block i with its x in xb; the next block's x goes to xn.  Returns false
+    // after the workgroup's last block (left unstored).  The two register
+    // sets swap roles from block to block (the loop below is unrolled by
+    // two), so no copy writes over the registers that the stores read.
+    auto block = [&](int i, Frag<T> (&xb)[PT][CK], Frag<T> (&xn)[PT][CK]) -> bool {
+        const int64_t p0 = pw + (int64_t)i * bstride;
+        const bool has_next = i + 1 < iters;
 #pragma unroll
         for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
             for (int pt = 0; pt < PT; ++pt) O[ct][pt] = f32x4{0.f, 0.f, 0.f, 0.f};
         bool ok = true;
-        for (int h = 0; h < H; ++h) {
-            if (h == 0 && pending) wait_vmcnt<Cfg::NXLOAD + Cfg::NSTORE>();
+        // One head of the block.  Head 0 is a separate call, so that the
+        // compiler's wait analysis sees the block start on its own: there the
+        // bias and the Z copies were retired before the previous block's
+        // stores, which stay in flight; at later heads this wave's Z_h copies
+        // and bias (issued during head h-1) are waited for here.
+        auto head = [&](int h, auto first) {
+            if constexpr (decltype(first)::value) wait_vmcnt<NSTORE>();
             else wait_vmcnt<0>();
             __syncthreads();  // every copy of Z_h landed; stage s^1 is no longer read
             f32x4 L[MT][PT];
@@ -330,20 +340,26 @@ __global__ __launch_bounds__(512, 1) void k_deslice_w8(const T *__restrict__ x, 
                         for (int pt = 0; pt < PT; ++pt) mma(L[mt][pt], a[kc & 1][mt], xb[pt][kc]);
                     if (kc + 1 < CK) __builtin_amdgcn_sched_group_barrier(0x100, MT, 0);  // next reads first
                     __builtin_amdgcn_sched_group_barrier(0x008, MT * PT, 0);
+                    // This head's share of the next block's x, once the first
+                    // K step has consumed the bias.
+                    if (kc == 0 && has_next) {
+                        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                        for (int j = 0; j < NXLOAD; ++j)
+                            if (xhead(j) == h) load_xfrag(p0 + bstride, j, xn);
+                    }
                 }
                 __builtin_amdgcn_sched_barrier(0);
             }
             // The next head's Z copies and bias (or head 0's of the next
-            // block): issued after the logits rather than at the barrier, where
-            // every wave would queue them at once.  One code path for both
-            // successors, so the compiler's wait counts see one issue point.
+            // block), after the logits rather than at the barrier, where every
+            // wave would queue them at once.
             if (h + 1 < H || has_next) {
                 const int hn = h + 1 < H ? h + 1 : 0;
                 stage_z(hn, stage ^ 1);
                 load_bias(hn, bias);
                 stage ^= 1;
             }
-            if (h + 1 == H && has_next) load_x(blk + gridDim.x, xb);  // younger than the copies above
             Frag<T> wf[PT][KM];
             ok = softmax_unshifted<T, MT, PT, KM>(L, wf) && ok;
             // Z fragments of channel tile ct+1 are read while tile ct's MFMAs run.
@@ -367,23 +383,45 @@ __global__ __launch_bounds__(512, 1) void k_deslice_w8(const T *__restrict__ x, 
                 }
                 __builtin_amdgcn_sched_barrier(0);
             }
-        }
-        if (ok) {
-            store_rows<T, CT, PT, C>(O, out, p0, n, g, li);
-        } else {
-            // Rare: a row's exp2 sum left the safe window.  This wave redoes
-            // its block from global-memory fragments with the shifted softmax
-            // (no barriers inside), 16 points at a time.
-            #pragma unroll 1
-            for (int pt = 0; pt < PT; ++pt)  // 16 points at a time keeps its registers small
-                deslice_block_global<T, C, M, 1>(x, n, p0 + 16 * pt, H, w2p, b2s, zp, out, lane);
-        }
-        // Only a full block on the fast path with a successor leaves exactly
-        // NXLOAD + NSTORE operations behind its last copies; otherwise drain.
-        pending = ok && has_next && p0 + 16 * PT <= n;
-        if (!pending) wait_vmcnt<0>();
+        };
+        head(0, std::true_type{});
+        for (int h = 1; h < H; ++h) head(h, std::false_type{});
+        if (!ok) failed |= 1ull << i;
+        if (!has_next) return false;
+        // Next block's x, its first Z copies and its first bias have all had
+        // at least part of a head to arrive; with them retired before the
+        // stores, nothing later has to wait for the stores.
+        wait_vmcnt<0>();
+        // Every block but a workgroup's last is full: exactly NSTORE stores,
+        // unconditionally (a failed block is rewritten below).
+#pragma unroll
+        for (int k = 0; k < CT / 2; ++k)
+#pragma unroll
+            for (int pt = 0; pt < PT; ++pt) {
+                const f32x4 &u = O[2 * k][pt], &v = O[2 * k + 1][pt];
+                *reinterpret_cast<bf16x8 *>(out + (size_t)(p0 + pt * 16 + li) * C + 32 * k + 8 * g) =
+                    bf16x8{(__bf16)u[0], (__bf16)u[1], (__bf16)u[2], (__bf16)u[3],
+                           (__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
+            }
+        return true;
+    };
+    for (int i = 0;; i += 2) {
+        if (!block(i, xA, xB)) break;
+        if (!block(i + 1, xB, xA)) break;
     }
+    // The workgroup's last block (possibly partial): masked stores.
+    if (!((failed >> (iters - 1)) & 1)) store_rows<T, CT, PT, C>(O, out, pw + (int64_t)(iters - 1) * bstride, n, g, li);
     wait_vmcnt<0>();
+    // Rare: blocks whose exp2 sums left the safe window, redone from
+    // global-memory fragments with the max-shifted softmax, 16 points at a
+    // time (no barriers).
+    while (failed) {
+        const int i = __builtin_ctzll(failed);
+        failed &= failed - 1;
+#pragma unroll 1
+        for (int pt = 0; pt < PT; ++pt)
+            deslice_block_global<T, C, M, 1>(x, n, pw + (int64_t)i * bstride + 16 * pt, H, w2p, b2s, zp, out, lane);
+    }
 }
 
 }  // namespace ts3
