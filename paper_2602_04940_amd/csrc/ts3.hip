@@ -14,6 +14,7 @@
 #include "../../include/ts3.h"
 #include "ts3_pass1.h"
 #include "ts3_pass1w8.h"
+#include "ts3_pass1g2.h"
 #include "ts3_pass2.h"
 #include "ts3_small.h"
 
@@ -65,8 +66,14 @@ template <typename T, int C, int M>
 void launch_pass1(const void *x, int64_t n, int64_t span0, int32_t Q, int32_t nspan, int32_t H,
                   const void *w2p, const float *b2s, float *partials, hipStream_t st) {
     if constexpr (sizeof(T) == 2 && M >= 32 && C == 128) {
-        hipLaunchKernelGGL((k_slice_accumulate_w8<C, M>), dim3(nspan * H), dim3(512), 0, st,
-                           (const bf16_t *)x, n, span0, Q, nspan, H, (const bf16_t *)w2p, b2s, partials);
+        // Two heads per workgroup whenever H is even (independently of the
+        // span count, so that every tiling sums a span the same way).
+        if (H % 2 == 0)
+            hipLaunchKernelGGL((k_slice_accumulate_g2<C, M>), dim3(nspan * (H / 2)), dim3(512), 0, st,
+                               (const bf16_t *)x, n, span0, Q, nspan, H, (const bf16_t *)w2p, b2s, partials);
+        else
+            hipLaunchKernelGGL((k_slice_accumulate_w8<C, M>), dim3(nspan * H), dim3(512), 0, st,
+                               (const bf16_t *)x, n, span0, Q, nspan, H, (const bf16_t *)w2p, b2s, partials);
     } else {
         hipLaunchKernelGGL((k_slice_accumulate<T, C, M>), dim3(nspan * H), dim3(256), 0, st,
                            (const T *)x, n, span0, Q, nspan, H, (const T *)w2p, b2s, partials);

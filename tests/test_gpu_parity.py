@@ -127,6 +127,31 @@ def test_shapes_ragged_tiles_random_biases(C, H, M, dtype):
             assert rel_l2(st[k], ref_st[k]) <= BF16_TOL, k
 
 
+@pytest.mark.parametrize("Q", [96, 100])
+def test_bf16_two_head_workgroups_odd_block_counts(Q):
+    """Pass 1 with two heads per workgroup: a span of Q = 96 points has three
+    32-point blocks, so the second block stream's last step has no points;
+    Q = 100 leaves it 4.  States match the oracle and tiled runs match an
+    untiled one bitwise."""
+    C, H, M, N = 128, 8, 64, 4100
+    banner(f"two-head pass 1, Q={Q}, N={N}")
+    rng = np.random.default_rng(Q)
+    from ts3_synth import round_bf16
+    x = round_bf16(rng.standard_normal((N, C)))
+    W = make_weights(C, H, M, C // H, seed=7, bias_seed=8)
+    got, st, out_t = _run(x, W, C, H, M, "bf16", 0.5, 10 * Q, 1000, Q)
+    ref = oracle.layer_forward_fast(x, W, H, M, 2.0)
+    ref_st = oracle.build_state(x, W, H, M, 2.0)
+    assert rel_l2(got, ref) <= BF16_TOL
+    for k in ("s_raw", "d", "Z"):
+        assert rel_l2(st[k], ref_st[k]) <= BF16_TOL, k
+    one_tile = -(-N // Q) * Q
+    got1, st1, out_1 = _run(x, W, C, H, M, "bf16", 0.5, one_tile, N, Q)
+    for k in ("s_raw", "d", "Z"):
+        assert np.array_equal(st1[k], st[k]), k
+    assert np.array_equal(got1, got)
+
+
 # ------------------------------------------------------------ special cases
 
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])

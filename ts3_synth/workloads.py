@@ -45,7 +45,7 @@ WORKLOADS = {
                              "bf16", 1_000_000, 1_000_000, 31_250),
     # cached-state inference over 100M volume points, 1M-point tiles and chunks
     "volume_100m_bf16": Workload("volume_100m_bf16", "volume", 4, 100_000_000, 128, 8, 64, 16, 0.5,
-                                 "bf16", 1_000_000, 1_000_000, 31_250),
+                                 "bf16", 1_000_000, 1_000_000, 15_625),
 }
 
 
