@@ -146,7 +146,10 @@ ts3_status ts3_deslice(const ts3_state *st, const ts3_weights *w, const void *x_
 /* Whole layer on a resident mesh (Algorithm 1): reset, accumulate tiles of
  * `tile` points, finalize, attention, deslice chunks of `chunk` points.
  * tile must be a multiple of group_span; N <= max_points.  Allocates nothing.
- * Leaves the state ATTENDED. */
+ * Consecutive tiles (and chunks) are enqueued alternately on `stream` and on
+ * a second stream that the state owns, forked from `stream` by an event and
+ * joined back into it before the call returns: work enqueued on `stream`
+ * afterwards sees the whole layer.  Leaves the state ATTENDED. */
 ts3_status ts3_layer_forward(ts3_state *st, const ts3_weights *w, const void *x, int64_t N,
                              int64_t tile, int64_t chunk, void *out, void *stream);
 

@@ -175,6 +175,12 @@ struct ts3_state {
     int phase = PH_RESET;
     bool w2_ready = false;
     const float *W2 = nullptr, *b2 = nullptr;
+    // Second stream for ts3_layer_forward (default priority): consecutive
+    // tiles and chunks alternate between it and the caller's stream, so one
+    // launch's last partial round of workgroups overlaps the next launch's
+    // first.
+    hipStream_t aux = nullptr;
+    hipEvent_t ev_fork = nullptr, ev_join = nullptr;
 };
 
 namespace {
@@ -274,10 +280,24 @@ ts3_status ts3_state_free(ts3_state *st) {
                     st->Z,        st->b2s,  st->b3,    st->w2p,  st->zp};
     for (void *b : bufs)
         if (b) (void)hipFree(b);
+    if (st->ev_fork) (void)hipEventDestroy(st->ev_fork);
+    if (st->ev_join) (void)hipEventDestroy(st->ev_join);
+    if (st->aux) (void)hipStreamDestroy(st->aux);
     delete st;
     if (e != hipSuccess) return fail(TS3_ERR_HIP, "hipDeviceSynchronize: %s", hipGetErrorString(e));
     return TS3_OK;
 }
+
+namespace {
+// The second stream and its two events, made with the state so that
+// ts3_layer_forward creates nothing.
+ts3_status make_aux(ts3_state *st) {
+    HIP_TRY(hipStreamCreateWithFlags(&st->aux, hipStreamNonBlocking));
+    HIP_TRY(hipEventCreateWithFlags(&st->ev_fork, hipEventDisableTiming));
+    HIP_TRY(hipEventCreateWithFlags(&st->ev_join, hipEventDisableTiming));
+    return TS3_OK;
+}
+}  // namespace
 
 ts3_status ts3_state_create(const ts3_desc *desc, ts3_state **out) {
     if (!out) return fail(TS3_ERR_INVALID_ARG, "out is NULL");
@@ -322,6 +342,11 @@ ts3_status ts3_state_create(const ts3_desc *desc, ts3_state **out) {
         st->bytes += r.bytes;
     }
     st->span_written.assign((size_t)st->nspan_max, 0);
+    s = make_aux(st);
+    if (s != TS3_OK) {
+        ts3_state_free(st);
+        return s;
+    }
     *out = st;
     return TS3_OK;
 }
@@ -470,6 +495,27 @@ ts3_status ts3_deslice(const ts3_state *st, const ts3_weights *w, const void *x_
     return TS3_OK;
 }
 
+namespace {
+
+// The second stream starts after everything enqueued on `main` so far.
+ts3_status fork_aux(ts3_state *st, hipStream_t main, bool *forked) {
+    HIP_TRY(hipEventRecord(st->ev_fork, main));
+    HIP_TRY(hipStreamWaitEvent(st->aux, st->ev_fork, 0));
+    *forked = true;
+    return TS3_OK;
+}
+
+// Later work on `main` waits for everything enqueued on the second stream
+// (also after an error, so nothing is left running unordered).
+ts3_status join_aux(ts3_state *st, hipStream_t main, ts3_status s) {
+    hipError_t e = hipEventRecord(st->ev_join, st->aux);
+    if (e == hipSuccess) e = hipStreamWaitEvent(main, st->ev_join, 0);
+    if (e != hipSuccess && s == TS3_OK) return fail(TS3_ERR_HIP, "stream join: %s", hipGetErrorString(e));
+    return s;
+}
+
+}  // namespace
+
 ts3_status ts3_layer_forward(ts3_state *st, const ts3_weights *w, const void *x, int64_t N, int64_t tile,
                              int64_t chunk, void *out, void *stream) {
     if (!st) return fail(TS3_ERR_INVALID_ARG, "state is NULL");
@@ -479,17 +525,28 @@ ts3_status ts3_layer_forward(ts3_state *st, const ts3_weights *w, const void *x,
                     (long long)st->desc.group_span);
     if (N > 0 && (!x || !out)) return fail(TS3_ERR_INVALID_ARG, "x or out is NULL");
     ts3_status s = ts3_state_reset(st, stream);
+    if (s == TS3_OK) s = check_weights_w2(w);
     const char *xb = (const char *)x;
     char *ob = (char *)out;
     const int64_t row = (int64_t)st->desc.C * st->esize;
-    for (int64_t t0 = 0; s == TS3_OK && t0 < N; t0 += tile)
-        s = ts3_slice_accumulate(st, w, xb + t0 * row, std::min(tile, N - t0), t0, stream);
-    if (s == TS3_OK && N == 0 && (!w || !w->W2)) s = check_weights_w2(w);
-    if (s == TS3_OK && !st->w2_ready) s = prep_w2(st, w, (hipStream_t)stream);
+    hipStream_t main = (hipStream_t)stream;
+    // W2' is prepared once on the caller's stream, before either stream reads it.
+    if (s == TS3_OK) s = prep_w2(st, w, main);
+    // Pass-1 tiles write disjoint group partials and pass-2 chunks disjoint
+    // output rows, so each loop runs its launches alternately on the caller's
+    // stream and the second one, forked from and joined back into the caller's.
+    bool forked = false;
+    if (s == TS3_OK && N > tile) s = fork_aux(st, main, &forked);
+    for (int64_t t0 = 0, i = 0; s == TS3_OK && t0 < N; t0 += tile, ++i)
+        s = ts3_slice_accumulate(st, w, xb + t0 * row, std::min(tile, N - t0), t0, (i & 1) ? st->aux : main);
+    if (forked) s = join_aux(st, main, s);
     if (s == TS3_OK) s = ts3_slice_finalize(st, w, stream);
     if (s == TS3_OK) s = ts3_token_attention(st, w, stream);
-    for (int64_t c0 = 0; s == TS3_OK && c0 < N; c0 += chunk)
-        s = ts3_deslice(st, w, xb + c0 * row, std::min(chunk, N - c0), ob + c0 * row, stream);
+    forked = false;
+    if (s == TS3_OK && N > chunk) s = fork_aux(st, main, &forked);
+    for (int64_t c0 = 0, i = 0; s == TS3_OK && c0 < N; c0 += chunk, ++i)
+        s = ts3_deslice(st, w, xb + c0 * row, std::min(chunk, N - c0), ob + c0 * row, (i & 1) ? st->aux : main);
+    if (forked) s = join_aux(st, main, s);
     return s;
 }
 
