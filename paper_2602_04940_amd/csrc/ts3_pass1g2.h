@@ -149,8 +149,20 @@ __global__ __launch_bounds__(512, 1) void k_slice_accumulate_g2(
     // (row bit 2), its contraction slices the tiles hf*MTH .. hf*MTH+MTH-1.
     const uint32_t xbase = (uint32_t)(stream * NSX * XTILE);
     const uint32_t wbase = (uint32_t)(Cfg::X_BYTES + pair * NSW * WTILE);
-    uint32_t xl0 = xbase + xoff<XROW>(prow(hf, li), 16 * g);
-    uint32_t xt0 = xbase + xoff<XROW>(8 * g + (li >> 2), 8 * (li & 3));
+    const uint32_t xl0 = xbase + xoff<XROW>(prow(hf, li), 16 * g);
+    const uint32_t xt0 = xbase + xoff<XROW>(8 * g + (li >> 2), 8 * (li & 3));
+    // The x-tile addresses of every K step (logits) and channel tile
+    // (contraction), computed once and held in registers: an XOR in front
+    // of each read costs more than the registers.
+    static_assert(CK == 4 && CT == 8, "the address sets below are written for C = 128");
+    uint32_t xl1 = xl0 ^ (1 << 6), xl2 = xl0 ^ (2 << 6), xl3 = xl0 ^ (3 << 6);
+    uint32_t xt1 = xt0 ^ (1 << 5), xt2 = xt0 ^ (2 << 5), xt3 = xt0 ^ (3 << 5), xt4 = xt0 ^ (4 << 5),
+             xt5 = xt0 ^ (5 << 5), xt6 = xt0 ^ (6 << 5), xt7 = xt0 ^ (7 << 5);
+    uint32_t xl0v = xl0, xt0v = xt0;
+    auto xl_at = [&](int kc) { return kc == 0 ? xl0v : kc == 1 ? xl1 : kc == 2 ? xl2 : xl3; };
+    auto xt_at = [&](int ct) {
+        return ct == 0 ? xt0v : ct == 1 ? xt1 : ct == 2 ? xt2 : ct == 3 ? xt3 : ct == 4 ? xt4 : ct == 5 ? xt5 : ct == 6 ? xt6 : xt7;
+    };
     uint32_t wt0 = wbase + woff<WROW>(8 * g + (li >> 2), 8 * (li & 3));
     uint32_t ws0 = wbase + woff<WROW>(prow(hf, li), 8 * g);
 
@@ -160,12 +172,12 @@ __global__ __launch_bounds__(512, 1) void k_slice_accumulate_g2(
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) L[mt] = bias[mt];
         Frag<T> xb[2];
-        xb[0].v = *reinterpret_cast<const bf16x8 *>(lds + xl0 + SL * XTILE);
+        xb[0].v = *reinterpret_cast<const bf16x8 *>(lds + xl_at(0) + SL * XTILE);
 #pragma unroll
         for (int kc = 0; kc < CK; ++kc) {
             __builtin_amdgcn_sched_barrier(0);
             if (kc + 1 < CK)
-                xb[(kc + 1) & 1].v = *reinterpret_cast<const bf16x8 *>(lds + (xl0 ^ ((kc + 1) << 6)) + SL * XTILE);
+                xb[(kc + 1) & 1].v = *reinterpret_cast<const bf16x8 *>(lds + xl_at(kc + 1) + SL * XTILE);
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) mma(L[mt], w2[mt][kc], xb[kc & 1]);
             if (kc + 1 < CK) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
@@ -181,7 +193,7 @@ __global__ __launch_bounds__(512, 1) void k_slice_accumulate_g2(
     };
     auto read_b = [&](auto slot, int ct, Frag<T> &b) {
         constexpr int SL = decltype(slot)::value;
-        tr_frag<XROW>(b, lds + (xt0 ^ (ct << 5)) + SL * XTILE);
+        tr_frag<XROW>(b, lds + xt_at(ct) + SL * XTILE);
     };
     auto contract = [&](auto slot, auto wslot) {
         Frag<T> a[MTH], b;
@@ -217,7 +229,8 @@ __global__ __launch_bounds__(512, 1) void k_slice_accumulate_g2(
     auto step = [&](int j, auto slot, auto wslot) {
         constexpr int SL = decltype(slot)::value, SW = decltype(wslot)::value;
         constexpr int PREV = (SL + NSX - 1) % NSX, PREVW = (SW + NSW - 1) % NSW;
-        asm volatile("" : "+v"(xl0), "+v"(xt0), "+v"(wt0), "+v"(ws0));
+        asm volatile("" : "+v"(xl0v), "+v"(xl1), "+v"(xl2), "+v"(xl3), "+v"(wt0), "+v"(ws0));
+        asm volatile("" : "+v"(xt0v), "+v"(xt1), "+v"(xt2), "+v"(xt3), "+v"(xt4), "+v"(xt5), "+v"(xt6), "+v"(xt7));
         const bool row_valid = prow(hf, li) < block_valid(j);
         Frag<T> a[MTH], b;
         read_a(ic<PREVW>{}, a);
