@@ -44,29 +44,6 @@ __device__ __forceinline__ void pack_weights(const f32x4 (&E)[MT][PT], int pt, f
         }
 }
 
-// Fast path: exp2 of the logits without a shift.  Returns false (wave-uniform)
-// if any row's sum falls outside the safe window; L then holds exp2 values.
-template <typename T, int MT, int PT, int KM>
-__device__ __forceinline__ bool softmax_unshifted(f32x4 (&L)[MT][PT], Frag<T> (&wf)[PT][KM]) {
-    bool ok = true;
-#pragma unroll
-    for (int pt = 0; pt < PT; ++pt) {
-        float sum = 0.f;
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const float e = fast_exp2(L[mt][pt][r]);
-                L[mt][pt][r] = e;
-                sum += e;
-            }
-        sum = xrow_sum(sum);
-        ok = ok && softmax_sum_ok(sum);
-        pack_weights<T, MT, PT, KM>(L, pt, fast_rcp(sum), wf);
-    }
-    return !__any(!ok);
-}
-
 template <typename T, int MT, int PT, int KM>
 __device__ __forceinline__ void softmax_shifted(f32x4 (&L)[MT][PT], Frag<T> (&wf)[PT][KM]) {
 #pragma unroll
@@ -320,29 +297,46 @@ __global__ __launch_bounds__(512, 1) void k_deslice_w8(const T *__restrict__ x, 
 #pragma unroll
                 for (int pt = 0; pt < PT; ++pt) L[mt][pt] = bias[mt];
             const int cur = stage;
-            // K steps outermost: consecutive MFMAs go to the 2*MT independent
-            // accumulators instead of chaining on one; the W2' fragments of
-            // step kc+1 are read while step kc's MFMAs run.
+            // Slice tiles outermost: the exp2 of tile mt-1 (and their running
+            // row sums) ride between tile mt's MFMAs, where the transcendental
+            // unit runs beside the matrix core; the W2' fragment of step i+2
+            // is read while step i's MFMAs run.  The sums keep the order
+            // tile, then r, of the plain softmax.
+            float esum[PT];
+#pragma unroll
+            for (int pt = 0; pt < PT; ++pt) esum[pt] = 0.f;
+            auto exp_at = [&](int mt, int e) {
+                const int pt = e / 4, r = e % 4;
+                float v = fast_exp2(L[mt][pt][r]);
+                asm volatile("" : "+v"(v));
+                L[mt][pt][r] = v;
+                esum[pt] += v;
+            };
             {
+                constexpr int NSTEP = MT * CK, DIST = 2, EPS = (4 * PT) / CK;
+                static_assert((4 * PT) % CK == 0, "exp2 spread evenly over a tile's K steps");
                 const T *wh = w2l + (size_t)h * MT * CK * 512 + lane * 8;
-                Frag<T> a[2][MT];
+                Frag<T> a[4];
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt) load8(a[0][mt], wh + (mt * CK) * 512);
+                for (int i = 0; i < DIST; ++i) load8(a[i], wh + i * 512);
 #pragma unroll
-                for (int kc = 0; kc < CK; ++kc) {
+                for (int i = 0; i < NSTEP; ++i) {
+                    const int mt = i / CK, kc = i % CK;
                     __builtin_amdgcn_sched_barrier(0);
-                    if (kc + 1 < CK)
+                    if (i + DIST < NSTEP) load8(a[(i + DIST) & 3], wh + (i + DIST) * 512);
 #pragma unroll
-                        for (int mt = 0; mt < MT; ++mt) load8(a[(kc + 1) & 1][mt], wh + (mt * CK + kc + 1) * 512);
+                    for (int pt = 0; pt < PT; ++pt) mma(L[mt][pt], a[i & 3], xb[pt][kc]);
+                    if (mt > 0)
 #pragma unroll
-                    for (int mt = 0; mt < MT; ++mt)
+                        for (int e = kc * EPS; e < (kc + 1) * EPS; ++e) exp_at(mt - 1, e);
+                    if (i + DIST < NSTEP) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
 #pragma unroll
-                        for (int pt = 0; pt < PT; ++pt) mma(L[mt][pt], a[kc & 1][mt], xb[pt][kc]);
-                    if (kc + 1 < CK) __builtin_amdgcn_sched_group_barrier(0x100, MT, 0);  // next reads first
-                    __builtin_amdgcn_sched_group_barrier(0x008, MT * PT, 0);
-                    // This head's share of the next block's x, once the first
-                    // K step has consumed the bias.
-                    if (kc == 0 && has_next) {
+                    for (int q = 0; q < PT || q < EPS; ++q) {
+                        if (q < PT) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                        if (mt > 0 && q < EPS) __builtin_amdgcn_sched_group_barrier(0x400, 1, 0);
+                    }
+                    // This head's share of the next block's x, after the first tile.
+                    if (i == CK - 1 && has_next) {
                         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                         for (int j = 0; j < NXLOAD; ++j)
@@ -350,6 +344,8 @@ __global__ __launch_bounds__(512, 1) void k_deslice_w8(const T *__restrict__ x, 
                     }
                 }
                 __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int e = 0; e < 4 * PT; ++e) exp_at(MT - 1, e);
             }
             // The next head's Z copies and bias (or head 0's of the next
             // block), after the logits rather than at the barrier, where every
@@ -361,7 +357,16 @@ __global__ __launch_bounds__(512, 1) void k_deslice_w8(const T *__restrict__ x, 
                 stage ^= 1;
             }
             Frag<T> wf[PT][KM];
-            ok = softmax_unshifted<T, MT, PT, KM>(L, wf) && ok;
+            {   // the rest of the fast-path softmax: row sums across the four rows
+                bool okk = true;
+#pragma unroll
+                for (int pt = 0; pt < PT; ++pt) {
+                    const float sm = xrow_sum(esum[pt]);
+                    okk = okk && softmax_sum_ok(sm);
+                    pack_weights<T, MT, PT, KM>(L, pt, fast_rcp(sm), wf);
+                }
+                ok = !__any(!okk) && ok;
+            }
             // Z fragments of channel tile ct+1 are read while tile ct's MFMAs run.
             {
                 const T *zl = zs + (size_t)cur * Cfg::STAGE_ELEMS + lane * 8;
