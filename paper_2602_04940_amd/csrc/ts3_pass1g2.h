@@ -80,7 +80,8 @@ __global__ __launch_bounds__(512, 1) void k_slice_accumulate_g2(
 
     const int64_t p_begin = (int64_t)span_local * Q;
     const int64_t p_end = p_begin + Q < n_tile ? p_begin + Q : n_tile;
-    const int nblk = (int)((p_end - p_begin + 31) >> 5);
+    const int nrows = (int)(p_end - p_begin);  // <= Q <= 2^30
+    const int nblk = (nrows + 31) >> 5;
     const int nit = (nblk + 1) >> 1;  // block steps, the same for every wave
 
     unsigned char *const xring = lds + stream * NSX * XTILE;
@@ -95,12 +96,13 @@ __global__ __launch_bounds__(512, 1) void k_slice_accumulate_g2(
         const int R = i * Cfg::ROWS_PER_LOAD + lane / NCH;
         return (uint32_t)(R * XROW + (((lane % NCH) ^ xswz<XROW>(R)) << 4));
     };
+    // Row offsets within the span are 32-bit; only the global base is 64-bit.
     auto issue_x = [&](int j, auto slot) {
         constexpr int SL = decltype(slot)::value;
-        const int64_t p0 = p_begin + ((int64_t)(stream + 2 * j) << 5);
+        const int r0 = (stream + 2 * j) << 5;
         const uint32_t dst = xring_lds + SL * XTILE;
-        if (p0 + 32 <= p_end) {
-            const void *base = x + p0 * C;
+        if (__builtin_expect(r0 + 32 <= nrows, 1)) {
+            const void *base = x + (p_begin + r0) * C;
 #pragma unroll
             for (int kk = 0; kk < MY_LOADS; ++kk) {
                 const int i = 2 * (2 * hsel + kk) + hf;
@@ -112,9 +114,8 @@ __global__ __launch_bounds__(512, 1) void k_slice_accumulate_g2(
                 const int i = 2 * (2 * hsel + kk) + hf;
                 const int R = i * Cfg::ROWS_PER_LOAD + lane / NCH;
                 const int ch = (lane % NCH) ^ xswz<XROW>(R);
-                int64_t p = p0 + R;
-                p = p < p_end ? p : p_end - 1;
-                dma16(reinterpret_cast<const unsigned char *>(x + (size_t)p * C) + ch * 16, dst + i * 1024);
+                const int r = r0 + R < nrows ? r0 + R : nrows - 1;
+                dma16(reinterpret_cast<const unsigned char *>(x + (size_t)(p_begin + r) * C) + ch * 16, dst + i * 1024);
             }
         }
     };
@@ -217,8 +218,8 @@ __global__ __launch_bounds__(512, 1) void k_slice_accumulate_g2(
                        (__bf16)(E[mt][3] * inv)};
     };
     auto block_valid = [&](int j) {
-        const int64_t left = p_end - (p_begin + ((int64_t)(stream + 2 * j) << 5));
-        return (int)(left <= 0 ? 0 : left < 32 ? left : 32);
+        const int left = nrows - ((stream + 2 * j) << 5);
+        return left <= 0 ? 0 : left < 32 ? left : 32;
     };
 
     // Step j (block j of the stream, x slot SL = j % NSX, w slot SW = j % NSW):
