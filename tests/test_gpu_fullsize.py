@@ -1,6 +1,6 @@
 """Parity at the benchmark's full size: the 100M-point volume mesh, C=128, H=8,
 M=64, bf16, in the launch configuration bench.py times (1M-point tiles and
-decode chunks, group span 31,250).
+decode chunks, group span 15,625).
 
 The float64 oracle cannot redo pass 1 over 1e8 points in test time, so pass 1
 is checked through properties that hold at any size, with error bounds derived
