@@ -102,7 +102,7 @@ def summarize_traffic(fetch_dir: str, write_dir: str, command: str):
         factor = CAL_BYTES / (float(cal["Counter_Value"]) * 1024.0)
         out.setdefault("calibration", {})[name] = {"copy_bytes": CAL_BYTES, "counter_kib": float(cal["Counter_Value"]),
                                                   "bytes_per_counted_byte": factor}
-        for kname in ("k_slice_accumulate_g2", "k_deslice_w8"):
+        for kname in ("k_slice_accumulate_pc", "k_deslice_w8"):
             vals = [float(r["Counter_Value"]) for r in rs if kname + "<" in r["Kernel_Name"]]
             per.setdefault(kname, {})[name] = (sum(vals) / len(vals), len(vals), factor)
     for kname, d in per.items():
@@ -224,7 +224,7 @@ def main():
 
     flop_per_point = 4 * wl.C * wl.H * wl.M        # logits + contraction, per pass
     if t_p1 >= t_p2:
-        kname, t_launch, nl = "k_slice_accumulate_g2", t_p1 / ntile, ntile
+        kname, t_launch, nl = "k_slice_accumulate_pc", t_p1 / ntile, ntile
     else:
         kname, t_launch, nl = "k_deslice_w8", t_p2 / nchunk, nchunk
     pts_launch = min(wl.tile, N)

@@ -14,7 +14,7 @@
 #include "../../include/ts3.h"
 #include "ts3_pass1.h"
 #include "ts3_pass1w8.h"
-#include "ts3_pass1g2.h"
+#include "ts3_pass1pc.h"
 #include "ts3_pass2.h"
 #include "ts3_small.h"
 
@@ -69,7 +69,7 @@ void launch_pass1(const void *x, int64_t n, int64_t span0, int32_t Q, int32_t ns
         // Two heads per workgroup whenever H is even (independently of the
         // span count, so that every tiling sums a span the same way).
         if (H % 2 == 0)
-            hipLaunchKernelGGL((k_slice_accumulate_g2<C, M>), dim3(nspan * (H / 2)), dim3(512), 0, st,
+            hipLaunchKernelGGL((k_slice_accumulate_pc<C, M>), dim3(nspan * (H / 2)), dim3(512), 0, st,
                                (const bf16_t *)x, n, span0, Q, nspan, H, (const bf16_t *)w2p, b2s, partials);
         else
             hipLaunchKernelGGL((k_slice_accumulate_w8<C, M>), dim3(nspan * H), dim3(512), 0, st,
