@@ -327,19 +327,21 @@ __global__ __launch_bounds__(512, 1) void k_slice_accumulate_pc(
         auto wa_at = [&](int mt) { return mt == 0 ? wa0 : mt == 1 ? wa1 : mt == 2 ? wa2 : wa3; };
         // Contraction of the block in x slot SL and w slot SW; the xT fragment
         // of channel tile ct+1 is read while tile ct's MFMAs run.
-        auto contract = [&](auto slot, auto wslot) {
-            constexpr int SL = decltype(slot)::value, SW = decltype(wslot)::value;
+        // Contraction of the block in x slot sl and w slot sw (constants in the
+        // loop, so the slot offsets become immediates; the last block's are
+        // run-time values, one code path instead of one per slot).
+        auto contract = [&](int sl, int sw) {
             Frag<T> a[MT], b;
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt) tr_frag<WROW>(a[mt], lds + wa_at(mt) + SW * WTILE);
-            tr_frag<XROW>(b, lds + xt_at(0) + SL * XTILE);
+            for (int mt = 0; mt < MT; ++mt) tr_frag<WROW>(a[mt], lds + wa_at(mt) + sw * WTILE);
+            tr_frag<XROW>(b, lds + xt_at(0) + sl * XTILE);
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) mma(D[mt], a[mt], ones);
 #pragma unroll
             for (int ct = 0; ct < CT; ++ct) {
                 Frag<T> bn;
-                if (ct + 1 < CT) tr_frag<XROW>(bn, lds + xt_at(ct + 1) + SL * XTILE);
+                if (ct + 1 < CT) tr_frag<XROW>(bn, lds + xt_at(ct + 1) + sl * XTILE);
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) mma(S[mt][ct], a[mt], b);
                 b = bn;
@@ -351,15 +353,13 @@ __global__ __launch_bounds__(512, 1) void k_slice_accumulate_pc(
             constexpr int PREV = (SL + NSX - 1) % NSX, PREVW = (SW + NSW - 1) % NSW;
             asm volatile("" : "+v"(xt0), "+v"(xt1), "+v"(xt2), "+v"(xt3), "+v"(xt4), "+v"(xt5), "+v"(xt6), "+v"(xt7));
             asm volatile("" : "+v"(wa0), "+v"(wa1), "+v"(wa2), "+v"(wa3));
-            contract(ic<PREV>{}, ic<PREVW>{});  // block j-1
+            contract(PREV, PREVW);  // block j-1
             end_step(j, ic<PREV>{}, ic<1>{});
         };
         run_steps(step);
-        switch ((nit + NSX - 1) % NSX) {  // the last block (slots 3 and 1 if there was none)
-            case 0: contract(ic<0>{}, ic<0>{}); break;
-            case 1: contract(ic<1>{}, ic<1>{}); break;
-            case 2: contract(ic<2>{}, ic<0>{}); break;
-            default: contract(ic<3>{}, ic<1>{}); break;
+        {   // the last block (slots 3 and 1 if there was none)
+            const int last = (nit + NSX - 1) % NSX;
+            contract(last, last & 1);
         }
         __syncthreads();  // the pipeline's LDS becomes the reduction buffer
         float *mine = red + (size_t)pair * M * (C + 1);
