@@ -91,6 +91,16 @@ typedef struct {
 
 typedef struct ts3_state ts3_state; /* opaque */
 
+/* Gradients written by ts3_layer_backward: DEVICE pointers, float32, the
+ * layouts of the matching ts3_weights members; all nine must be non-NULL.
+ * They are overwritten, not accumulated into. */
+typedef struct {
+    float *dW2, *db2;
+    float *dW1, *db1;
+    float *dWq, *dWk, *dWv;
+    float *dW3, *db3;
+} ts3_grads;
+
 /* Which buffer ts3_state_get / ts3_state_set address (float32, row-major). */
 typedef enum {
     TS3_S_RAW = 0, /* [H, M, C]  sum_i w_i x_i            (valid after finalize) */
@@ -152,6 +162,21 @@ ts3_status ts3_deslice(const ts3_state *st, const ts3_weights *w, const void *x_
  * afterwards sees the whole layer.  Leaves the state ATTENDED. */
 ts3_status ts3_layer_forward(ts3_state *st, const ts3_weights *w, const void *x, int64_t N,
                              int64_t tile, int64_t chunk, void *out, void *stream);
+
+/* Backward of the layer (section 3.2: the training loop checkpoints every
+ * tile, so the slice weights are recomputed tile by tile, never stored).
+ * Given the output gradient g = dL/dx_out [N, C], writes dx = dL/dx [N, C]
+ * and the weight gradients.  The state must hold the forward of the same x
+ * and weights (ts3_layer_forward, or accumulate/finalize/attention over all N
+ * points): it supplies s_raw, d, s, s' and Z.  Three passes over the points,
+ * in tiles of `tile` points (a multiple of group_span): dZ = sum_i w_i^T g_i;
+ * then, after the token-side backward (Linear3, attention, Linear1, d^-1),
+ * dW2 and db2; then dx.  Sums over points are folded in index order, so the
+ * result does not depend on `tile`.  Float32 storage only
+ * (TS3_ERR_UNSUPPORTED for bfloat16).  x, g, dx are 16-byte aligned device
+ * pointers of N*C floats.  Allocates nothing; leaves the state ATTENDED. */
+ts3_status ts3_layer_backward(ts3_state *st, const ts3_weights *w, const void *x, const void *g, int64_t N,
+                              int64_t tile, void *dx, const ts3_grads *grads, void *stream);
 
 /* Copy a state buffer to host memory (n floats, must equal its size) after
  * synchronising `stream`.  For tests and inspection. */

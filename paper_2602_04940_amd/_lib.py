@@ -27,6 +27,13 @@ class Weights(ct.Structure):
 
 WEIGHT_NAMES = [n for n, _ in Weights._fields_]
 
+
+class Grads(ct.Structure):
+    _fields_ = [(n, ct.c_void_p) for n in ("dW2", "db2", "dW1", "db1", "dWq", "dWk", "dWv", "dW3", "db3")]
+
+
+GRAD_NAMES = [n for n, _ in Grads._fields_]
+
 _P = ct.c_void_p
 # name -> (restype, argtypes); must match include/ts3.h
 SIGNATURES = {
@@ -39,6 +46,8 @@ SIGNATURES = {
     "ts3_token_attention": (ct.c_int, [_P, ct.POINTER(Weights), _P]),
     "ts3_deslice": (ct.c_int, [_P, ct.POINTER(Weights), _P, ct.c_int64, _P, _P]),
     "ts3_layer_forward": (ct.c_int, [_P, ct.POINTER(Weights), _P, ct.c_int64, ct.c_int64, ct.c_int64, _P, _P]),
+    "ts3_layer_backward": (ct.c_int, [_P, ct.POINTER(Weights), _P, _P, ct.c_int64, ct.c_int64, _P,
+                                      ct.POINTER(Grads), _P]),
     "ts3_state_get": (ct.c_int, [_P, ct.c_int32, _P, ct.c_int64, _P]),
     "ts3_state_set": (ct.c_int, [_P, ct.POINTER(Weights), ct.c_int32, _P, ct.c_int64, _P, _P]),
     "ts3_status_string": (ct.c_char_p, [ct.c_int]),

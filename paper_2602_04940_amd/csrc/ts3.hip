@@ -15,6 +15,7 @@
 #include "ts3_pass1.h"
 #include "ts3_pass1w8.h"
 #include "ts3_pass1pc.h"
+#include "ts3_backward.h"
 #include "ts3_pass2.h"
 #include "ts3_small.h"
 
@@ -60,6 +61,12 @@ struct Kernels {
                   float *, hipStream_t);
     hipError_t (*pass2)(const void *, int64_t, int32_t, const void *, const float *, const void *, void *,
                         hipStream_t);
+    // Backward (float32 storage only; NULL for bfloat16).
+    void (*bw_head)(int, const float *, const float *, int64_t, int64_t, int32_t, int32_t, int32_t,
+                    const float *, const float *, const float *, const float *, const float *, float, float *,
+                    hipStream_t);
+    void (*bw_dx)(const float *, const float *, int64_t, int32_t, const float *, const float *, const float *,
+                  const float *, const float *, const float *, const float *, float, float *, hipStream_t);
 };
 
 template <typename T, int C, int M>
@@ -136,8 +143,31 @@ hipError_t launch_pass2(const void *x, int64_t n, int32_t H, const void *w2p, co
     return hipSuccess;
 }
 
+template <int C, int M>
+void launch_bw_head(int mode, const float *x, const float *g, int64_t n, int64_t span0, int32_t Q, int32_t nspan,
+                    int32_t H, const float *w2p, const float *b2s, const float *Z, const float *dsr,
+                    const float *dd, float inv_tau, float *partials, hipStream_t st) {
+    if (mode == 0)
+        hipLaunchKernelGGL((k_bw_head<C, M, 0>), dim3((unsigned)(nspan * H)), dim3(256), 0, st, x, g, n, span0, Q,
+                           nspan, H, w2p, b2s, Z, dsr, dd, inv_tau, partials);
+    else
+        hipLaunchKernelGGL((k_bw_head<C, M, 1>), dim3((unsigned)(nspan * H)), dim3(256), 0, st, x, g, n, span0, Q,
+                           nspan, H, w2p, b2s, Z, dsr, dd, inv_tau, partials);
+}
+
+template <int C, int M>
+void launch_bw_dx(const float *x, const float *g, int64_t n, int32_t H, const float *w2p, const float *b2s,
+                  const float *W2, const float *Z, const float *dsr, const float *dsT, const float *dd,
+                  float inv_tau, float *dx, hipStream_t st) {
+    hipLaunchKernelGGL((k_bw_dx<C, M>), dim3((unsigned)((n + 63) / 64)), dim3(256), 0, st, x, g, n, H, w2p, b2s,
+                       W2, Z, dsr, dsT, dd, inv_tau, dx);
+}
+
 template <typename T, int C, int M> Kernels make_kernels() {
-    return Kernels{&launch_pass1<T, C, M>, &launch_pass2<T, C, M>};
+    if constexpr (sizeof(T) == 4)
+        return Kernels{&launch_pass1<T, C, M>, &launch_pass2<T, C, M>, &launch_bw_head<C, M>, &launch_bw_dx<C, M>};
+    else
+        return Kernels{&launch_pass1<T, C, M>, &launch_pass2<T, C, M>, nullptr, nullptr};
 }
 
 bool find_kernels(int dtype, int C, int M, Kernels *k) {
@@ -167,6 +197,8 @@ struct ts3_state {
     // device buffers
     float *partials = nullptr, *runs = nullptr, *s_raw = nullptr, *dsum = nullptr, *s = nullptr,
           *s1 = nullptr, *Z = nullptr, *b2s = nullptr, *b3 = nullptr;
+    // backward: dZ, ds_raw [H][M][C], ds_raw transposed [H][C][M], dd [H][M], dW2^T [H][M][C]
+    float *bdZ = nullptr, *bdsr = nullptr, *bdsT = nullptr, *bdd = nullptr, *bdW2T = nullptr;
     void *w2p = nullptr, *zp = nullptr;
     int64_t bytes = 0;
     // host bookkeeping
@@ -276,8 +308,9 @@ const char *ts3_last_error(void) { return g_err.c_str(); }
 ts3_status ts3_state_free(ts3_state *st) {
     if (!st) return TS3_OK;
     hipError_t e = hipDeviceSynchronize();
-    void *bufs[] = {st->partials, st->runs, st->s_raw, st->dsum, st->s, st->s1,
-                    st->Z,        st->b2s,  st->b3,    st->w2p,  st->zp};
+    void *bufs[] = {st->partials, st->runs, st->s_raw, st->dsum, st->s,    st->s1,   st->Z,
+                    st->b2s,      st->b3,   st->w2p,   st->zp,   st->bdZ,  st->bdsr, st->bdsT,
+                    st->bdd,      st->bdW2T};
     for (void *b : bufs)
         if (b) (void)hipFree(b);
     if (st->ev_fork) (void)hipEventDestroy(st->ev_fork);
@@ -330,6 +363,11 @@ ts3_status ts3_state_create(const ts3_desc *desc, ts3_state **out) {
         {(void **)&st->b3, (int64_t)d.C * 4},
         {&st->w2p, (int64_t)d.H * (d.M / 16) * (d.C / 32) * 512 * st->esize},
         {&st->zp, (int64_t)d.H * (d.C / 16) * KM * 512 * st->esize},
+        {(void **)&st->bdZ, HM * d.C * 4},
+        {(void **)&st->bdsr, HM * d.C * 4},
+        {(void **)&st->bdsT, HM * d.C * 4},
+        {(void **)&st->bdd, HM * 4},
+        {(void **)&st->bdW2T, HM * d.C * 4},
     };
     for (auto &r : reqs) {
         hipError_t e = hipMalloc(r.p, (size_t)r.bytes);
@@ -548,6 +586,92 @@ ts3_status ts3_layer_forward(ts3_state *st, const ts3_weights *w, const void *x,
         s = ts3_deslice(st, w, xb + c0 * row, std::min(chunk, N - c0), ob + c0 * row, (i & 1) ? st->aux : main);
     if (forked) s = join_aux(st, main, s);
     return s;
+}
+
+namespace {
+
+// Ordered fold of the first nspan span partials into main [H*M*C] and the
+// column C entries into col [H*M] (the forward's fold kernels).
+ts3_status fold_partials(ts3_state *st, int64_t nspan, float *main, float *col, hipStream_t hs) {
+    const int64_t E = st->E;
+    const int64_t nrun = (nspan + FOLD - 1) / FOLD;
+    const unsigned gx = (unsigned)((E + 255) / 256);
+    hipLaunchKernelGGL(k_fold_runs, dim3(gx, (unsigned)nrun), dim3(256), 0, hs, st->partials, E, nspan, st->runs);
+    LAUNCH_CHECK("fold_runs");
+    hipLaunchKernelGGL(k_fold_final, dim3(gx), dim3(256), 0, hs, st->runs, E, nrun, st->desc.C, main, col);
+    LAUNCH_CHECK("fold_final");
+    return TS3_OK;
+}
+
+}  // namespace
+
+ts3_status ts3_layer_backward(ts3_state *st, const ts3_weights *w, const void *x, const void *g, int64_t N,
+                              int64_t tile, void *dx, const ts3_grads *gr, void *stream) {
+    if (!st) return fail(TS3_ERR_INVALID_ARG, "state is NULL");
+    if (!w || !w->W2 || !w->W1 || !w->Wq || !w->Wk || !w->Wv || !w->W3)
+        return fail(TS3_ERR_INVALID_ARG, "weights or a weight matrix is NULL");
+    if (!gr || !gr->dW2 || !gr->db2 || !gr->dW1 || !gr->db1 || !gr->dWq || !gr->dWk || !gr->dWv || !gr->dW3 ||
+        !gr->db3)
+        return fail(TS3_ERR_INVALID_ARG, "grads or one of its pointers is NULL");
+    const ts3_desc &d = st->desc;
+    if (d.io_dtype != TS3_FP32 || !st->k.bw_head || !st->k.bw_dx)
+        return fail(TS3_ERR_UNSUPPORTED, "the backward is built for float32 storage");
+    if (N <= 0 || tile <= 0) return fail(TS3_ERR_INVALID_ARG, "N > 0 and tile > 0 required");
+    if (tile % d.group_span != 0)
+        return fail(TS3_ERR_INVALID_ARG, "tile %lld is not a multiple of group_span %lld", (long long)tile,
+                    (long long)d.group_span);
+    if (N > d.max_points) return fail(TS3_ERR_INVALID_ARG, "N exceeds max_points");
+    if (!x || !g || !dx) return fail(TS3_ERR_INVALID_ARG, "x, g or dx is NULL");
+    if (((uintptr_t)x & 15) || ((uintptr_t)g & 15) || ((uintptr_t)dx & 15))
+        return fail(TS3_ERR_INVALID_ARG, "x, g and dx must be 16-byte aligned");
+    const int64_t Q = d.group_span;
+    const int64_t nspan_all = (N + Q - 1) / Q;
+    if (st->phase != PH_ATTEND || st->span_hi != nspan_all)
+        return fail(TS3_ERR_BAD_STATE, "backward needs the state of the forward over the same %lld points",
+                    (long long)N);
+    if (!same_w2(st, w)) return fail(TS3_ERR_INVALID_ARG, "W2/b2 differ from the ones of the forward");
+    hipStream_t hs = (hipStream_t)stream;
+    const float inv_tau = 1.f / d.temperature;
+    const int64_t HM = (int64_t)d.H * d.M;
+    const float *xf = (const float *)x, *gf = (const float *)g;
+    const float *w2p = (const float *)st->w2p;
+    auto head_pass = [&](int mode) -> ts3_status {
+        for (int64_t t0 = 0; t0 < N; t0 += tile) {
+            const int64_t nt = std::min(tile, N - t0);
+            st->k.bw_head(mode, xf + t0 * d.C, gf + t0 * d.C, nt, t0 / Q, (int32_t)Q, (int32_t)((nt + Q - 1) / Q),
+                          d.H, w2p, st->b2s, st->Z, st->bdsr, st->bdd, inv_tau, st->partials, hs);
+            LAUNCH_CHECK(mode == 0 ? "backward dZ pass" : "backward dW2 pass");
+        }
+        return TS3_OK;
+    };
+    // dZ = sum_i w_i^T g_i (its column C, sum_i w_i, is not needed)
+    ts3_status s = head_pass(0);
+    if (s == TS3_OK) s = fold_partials(st, nspan_all, st->bdZ, st->bdd, hs);
+    if (s != TS3_OK) return s;
+    // token side: ds_raw, dd and the Linear1 / attention / Linear3 gradients
+    const size_t lds = (size_t)(2 * d.M * d.C + 10 * d.M * d.dh + 2 * d.M * d.M) * 4;
+    if (lds > (size_t)ATTN_LDS_MAX) return fail(TS3_ERR_UNSUPPORTED, "token backward needs %zu bytes of LDS", lds);
+    static bool lds_set = false;
+    if (!lds_set) {
+        HIP_TRY(hipFuncSetAttribute((const void *)k_bw_token, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                    ATTN_LDS_MAX));
+        lds_set = true;
+    }
+    hipLaunchKernelGGL(k_bw_token, dim3(d.H), dim3(256), lds, hs, st->s_raw, st->dsum, st->s, st->s1, st->bdZ,
+                       w->W1, w->Wq, w->Wk, w->Wv, w->W3, d.C, d.H, d.M, d.dh, d.eps, st->bdsr, st->bdsT, st->bdd,
+                       gr->dW1, gr->db1, gr->dWq, gr->dWk, gr->dWv, gr->dW3, gr->db3);
+    LAUNCH_CHECK("token backward");
+    // dW2 (through its transpose per head) and db2
+    s = head_pass(1);
+    if (s == TS3_OK) s = fold_partials(st, nspan_all, st->bdW2T, gr->db2, hs);
+    if (s != TS3_OK) return s;
+    hipLaunchKernelGGL(k_bw_transpose_w2, dim3((unsigned)std::min<int64_t>((d.C * HM + 255) / 256, 4096)), dim3(256),
+                       0, hs, st->bdW2T, d.C, (int)HM, gr->dW2);
+    LAUNCH_CHECK("dW2 transpose");
+    // dx
+    st->k.bw_dx(xf, gf, N, d.H, w2p, st->b2s, w->W2, st->Z, st->bdsr, st->bdsT, st->bdd, inv_tau, (float *)dx, hs);
+    LAUNCH_CHECK("backward dx pass");
+    return TS3_OK;
 }
 
 ts3_status ts3_state_get(const ts3_state *st, int32_t which, float *host_dst, int64_t n, void *stream) {

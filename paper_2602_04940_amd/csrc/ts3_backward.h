@@ -1,0 +1,499 @@
+// Backward of the Physics-Attention layer for float32 storage, with the slice
+// weights recomputed tile by tile instead of stored: the paper trains with
+// every tile's slice computation checkpointed (section 3.2, "Geometry slice
+// tiling", and the Checkpoint steps of Algorithm 1).  Given the output
+// gradient g = dL/dx_out:
+//
+//   k_bw_head<MODE 0>  per (span, head): recompute w; partial dZ[m][:] =
+//                      sum_p w[p][m] g_p (and sum_p w in column C)
+//   k_bw_token         per head: back through Linear3, the attention among
+//                      the head's M tokens, Linear1 and the normalisation:
+//                      ds_raw, dd and the token-side weight gradients
+//   k_bw_head<MODE 1>  per (span, head): recompute w; dw = g.Z + x.ds_raw +
+//                      dd; dz = (1/tau) w (dw - sum_m w dw); partial
+//                      dW2^T[m][:] = sum_p dz[p][m] x_p and db2 = sum_p dz
+//   k_bw_dx            per 16-point wave block over all heads: recompute w
+//                      and dz; dx = sum_h dz W2_h^T + w ds_raw_h
+//
+// Span partials are folded in index order by the forward's fold kernels, so
+// every gradient is a fixed function of the inputs (any tiling, any run).
+// Contractions use the 16x16x4 float32 MFMA through the fragment helpers of
+// ts3_device.h (lane (row, g), slot t); A fragments are read from L2-resident
+// arrays, transposes go through per-wave LDS tiles.
+#pragma once
+#include "ts3_device.h"
+
+namespace ts3 {
+
+// Row-major [rows][K] float32 array -> A (or B) fragment whose lane row r and
+// slot (g, t) hold element [r][k0 + 8g + t]: 8 consecutive floats.
+__device__ __forceinline__ void frag_row(Frag<float> &f, const float *row_k0, int g) {
+    load8(f, row_k0 + 8 * g);
+}
+
+// Pack a [slices x points] register tile (lane (p, g) holds slices 16mt + 4g
+// + r of point p, tiles mt < MT) as the B operand of K32 step km: slot t holds
+// slice 32km + 16(t>>2) + 4g + (t&3); zero past M.
+template <int MT>
+__device__ __forceinline__ void pack_b(const f32x4 (&E)[MT], int km, Frag<float> &f) {
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+        const int mt = 2 * km + (t >> 2);
+        f.v[t] = mt < MT ? E[mt < MT ? mt : 0][t & 3] : 0.f;
+    }
+}
+
+// A fragment for the same K order from a row-major [rows][M] array: lane row
+// r, slot t holds [r][32km + 16(t>>2) + 4g + (t&3)] (zero past M).
+template <int M>
+__device__ __forceinline__ void frag_slices(Frag<float> &f, const float *row, int km, int g) {
+    const float4 a = *reinterpret_cast<const float4 *>(row + 32 * km + 4 * g);
+    f.v[0] = a.x; f.v[1] = a.y; f.v[2] = a.z; f.v[3] = a.w;
+    if (M >= 32) {
+        const float4 b = *reinterpret_cast<const float4 *>(row + 32 * km + 16 + 4 * g);
+        f.v[4] = b.x; f.v[5] = b.y; f.v[6] = b.z; f.v[7] = b.w;
+    } else {
+        f.v[4] = f.v[5] = f.v[6] = f.v[7] = 0.f;
+    }
+}
+
+// Max-shifted softmax over a head's M slices of one 16-point tile, in place
+// (E holds exp2-scaled logits); rows of invalid points become zero.
+template <int MT>
+__device__ __forceinline__ void softmax_tile(f32x4 (&E)[MT], bool valid) {
+    float mx = E[0][0];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) mx = fmaxf(mx, E[mt][r]);
+    mx = xrow_max(mx);
+    float sum = 0.f;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const float e = fast_exp2(E[mt][r] - mx);
+            E[mt][r] = e;
+            sum += e;
+        }
+    const float tot = xrow_sum(sum);  // every lane takes part in the cross-row swaps
+    const float inv = valid ? 1.f / tot : 0.f;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) E[mt][r] *= inv;
+}
+
+// Logits of head h for 16 points whose x rows start at xrow (lane row li):
+// E[mt] = b2s + W2'^T x, exp2-scaled (W2' = W2 log2(e) / tau).
+template <int C, int M>
+__device__ __forceinline__ void logits_tile(f32x4 (&E)[M / 16], const float *w2p, const float *b2s, int h,
+                                            const float *xrow, int lane) {
+    constexpr int MT = M / 16, CK = C / 32;
+    const int g = lane >> 4;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+        const float4 b = *reinterpret_cast<const float4 *>(b2s + h * M + mt * 16 + g * 4);
+        E[mt] = f32x4{b.x, b.y, b.z, b.w};
+    }
+    // K steps not unrolled: each step's fragments are loaded where they are
+    // used (unrolled, the compiler hoists them all and spills).
+#pragma unroll 1
+    for (int kc = 0; kc < CK; ++kc) {
+        Frag<float> xb;
+        frag_row(xb, xrow + 32 * kc, g);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            Frag<float> a;
+            load8(a, w2p + ((((size_t)h * MT + mt) * CK + kc) * 64 + lane) * 8);
+            mma(E[mt], a, xb);
+        }
+    }
+}
+
+// dw[m][p] = dd[h][m] + Z[h][m] . g_p + ds_raw[h][m] . x_p, then
+// dz = inv_tau * w * (dw - sum_m w dw) in place of dw (W holds w).
+template <int C, int M>
+__device__ __forceinline__ void dz_tile(f32x4 (&Dz)[M / 16], const f32x4 (&W)[M / 16], const float *Z,
+                                        const float *dsr, const float *dd, int h, const float *xrow,
+                                        const float *grow, float inv_tau, int lane) {
+    constexpr int MT = M / 16, CK = C / 32;
+    const int g = lane >> 4, li = lane & 15;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+        const float4 b = *reinterpret_cast<const float4 *>(dd + h * M + mt * 16 + g * 4);
+        Dz[mt] = f32x4{b.x, b.y, b.z, b.w};
+    }
+#pragma unroll 1
+    for (int kc = 0; kc < CK; ++kc) {
+        Frag<float> gb, xb;
+        frag_row(gb, grow + 32 * kc, g);
+        frag_row(xb, xrow + 32 * kc, g);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            const size_t row = ((size_t)h * M + mt * 16 + li) * C + 32 * kc;
+            Frag<float> a;
+            frag_row(a, Z + row, g);
+            mma(Dz[mt], a, gb);
+            frag_row(a, dsr + row, g);
+            mma(Dz[mt], a, xb);
+        }
+    }
+    float t = 0.f;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) t += W[mt][r] * Dz[mt][r];
+    t = xrow_sum(t);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) Dz[mt][r] = inv_tau * W[mt][r] * (Dz[mt][r] - t);
+}
+
+template <int C, int M> struct BwHeadCfg {
+    static constexpr int WAVES = 4;
+    static constexpr int TT = M * 32;  // floats of a wave's [M][32] tile of w^T (or dz^T)
+    static constexpr int RT = C * 32;  // floats of a wave's [C][32] tile of g^T (or x^T)
+    static constexpr int WAVE_FLOATS = TT + RT;
+    static constexpr int RED_FLOATS = WAVES * M * (C + 1);
+    static constexpr int LDS_BYTES =
+        4 * (WAVES * WAVE_FLOATS > RED_FLOATS ? WAVES * WAVE_FLOATS : RED_FLOATS);
+};
+
+// MODE 0: partials[span][h][m][c] = sum_p w[p][m] g[p][c], column C = sum_p w.
+// MODE 1: partials[span][h][m][c] = sum_p dz[p][m] x[p][c] (dW2^T rows of head
+//         h), column C = sum_p dz (db2).
+// One workgroup per (span, head), four waves; wave v takes the span's 32-point
+// blocks v, v+4, ...; the four wave accumulators are summed in a fixed order.
+// x, gout: tile bases [n_tile][C]; the tile starts on a span boundary.
+template <int C, int M, int MODE>
+__global__ __launch_bounds__(256, 1) void k_bw_head(const float *__restrict__ x, const float *__restrict__ gout,
+                                                    int64_t n_tile, int64_t span0, int32_t Q, int32_t nspan,
+                                                    int32_t H, const float *__restrict__ w2p,
+                                                    const float *__restrict__ b2s, const float *__restrict__ Z,
+                                                    const float *__restrict__ dsr, const float *__restrict__ dd,
+                                                    float inv_tau, float *__restrict__ partials) {
+    using Cfg = BwHeadCfg<C, M>;
+    constexpr int MT = M / 16, CT = C / 16;
+    __shared__ __attribute__((aligned(16))) float lds[Cfg::LDS_BYTES / 4];
+    const int span_local = (int)blockIdx.x / H, h = (int)blockIdx.x % H;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+    const int li = lane & 15, g = lane >> 4;
+    const int64_t p_begin = (int64_t)span_local * Q;
+    const int64_t p_end = p_begin + Q < n_tile ? p_begin + Q : n_tile;
+    const int nblk = (int)((p_end - p_begin + 31) >> 5);
+    float *tt = lds + wave * Cfg::WAVE_FLOATS;  // [M][32]: w^T or dz^T
+    float *rt = tt + Cfg::TT;                   // [C][32]: g^T or x^T
+    const float *R = MODE == 0 ? gout : x;      // the contraction's point rows
+
+    f32x4 S[MT][CT];
+    f32x4 D[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+        D[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) S[mt][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    Frag<float> ones;
+    ones8(ones);
+
+    for (int b = wave; b < nblk; b += Cfg::WAVES) {
+        const int64_t p0 = p_begin + ((int64_t)b << 5);
+        // w (MODE 0) or dz (MODE 1) of the block's two 16-point tiles, as the
+        // transposed tile tt[m][p].
+#pragma unroll
+        for (int pt = 0; pt < 2; ++pt) {
+            const int64_t p = p0 + 16 * pt + li;
+            const bool valid = p < p_end;
+            const int64_t pc = valid ? p : p_end - 1;  // padding rows repeat the last point
+            f32x4 E[MT];
+            logits_tile<C, M>(E, w2p, b2s, h, x + pc * C, lane);
+            softmax_tile<MT>(E, valid);
+            if constexpr (MODE == 1) {
+                f32x4 Dz[MT];
+                dz_tile<C, M>(Dz, E, Z, dsr, dd, h, x + pc * C, gout + pc * C, inv_tau, lane);
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) E[mt] = Dz[mt];
+            }
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) tt[(mt * 16 + g * 4 + r) * 32 + 16 * pt + li] = E[mt][r];
+        }
+        // The block's point rows, transposed: rt[c][p] (padding rows repeat the
+        // last point; their weights are zero).
+        for (int i = lane; i < 32 * (C / 4); i += 64) {
+            const int p = i / (C / 4), c4 = i % (C / 4);
+            const int64_t pp = p0 + p < p_end ? p0 + p : p_end - 1;
+            const float4 v = *reinterpret_cast<const float4 *>(R + pp * C + 4 * c4);
+            rt[(4 * c4 + 0) * 32 + p] = v.x;
+            rt[(4 * c4 + 1) * 32 + p] = v.y;
+            rt[(4 * c4 + 2) * 32 + p] = v.z;
+            rt[(4 * c4 + 3) * 32 + p] = v.w;
+        }
+        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's tile writes landed
+        __builtin_amdgcn_wave_barrier();
+        // S[m][c] += sum_p T[p][m] R[p][c] (K = the block's 32 points).
+        Frag<float> a[MT];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) frag_row(a[mt], tt + (mt * 16 + li) * 32, g);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) mma(D[mt], a[mt], ones);
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) {
+            Frag<float> bf;
+            frag_row(bf, rt + (ct * 16 + li) * 32, g);
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) mma(S[mt][ct], a[mt], bf);
+        }
+        __builtin_amdgcn_s_waitcnt(0xc07f);  // the tiles' reads are done before the next block rewrites them
+        __builtin_amdgcn_wave_barrier();
+    }
+
+    __syncthreads();
+    float *mine = lds + (size_t)wave * M * (C + 1);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int m = mt * 16 + g * 4 + r;
+#pragma unroll
+            for (int ct = 0; ct < CT; ++ct) mine[m * (C + 1) + ct * 16 + li] = S[mt][ct][r];
+            if (li == 0) mine[m * (C + 1) + C] = D[mt][r];
+        }
+    __syncthreads();
+    constexpr int E = M * (C + 1);
+    float *dst = partials + ((size_t)(span0 + span_local) * H + h) * E;
+    for (int e = threadIdx.x; e < E; e += 256)
+        dst[e] = (lds[e] + lds[E + e]) + (lds[2 * E + e] + lds[3 * E + e]);
+}
+
+// dx for 16-point wave blocks (four per workgroup): over the heads, recompute
+// w and dz, then dx[p][c] += sum_m dz[p][m] W2[c][hM+m] + w[p][m] ds_raw[h][m][c].
+// dsT is ds_raw transposed per head: [H][C][M].  W2 is the layer's (unscaled)
+// Linear2 weight [C][H*M].
+template <int C, int M>
+__global__ __launch_bounds__(256, 1) void k_bw_dx(const float *__restrict__ x, const float *__restrict__ gout,
+                                                  int64_t n, int32_t H, const float *__restrict__ w2p,
+                                                  const float *__restrict__ b2s, const float *__restrict__ W2,
+                                                  const float *__restrict__ Z, const float *__restrict__ dsr,
+                                                  const float *__restrict__ dsT, const float *__restrict__ dd,
+                                                  float inv_tau, float *__restrict__ dx) {
+    constexpr int MT = M / 16, CT = C / 16, KM = M >= 32 ? M / 32 : 1;
+    const int lane = threadIdx.x & 63;
+    const int wave = (int)(threadIdx.x >> 6);
+    const int li = lane & 15, g = lane >> 4;
+    const int64_t p0 = ((int64_t)blockIdx.x * 4 + wave) * 16;
+    if (p0 >= n) return;  // wave-uniform; the kernel has no barriers
+    const int64_t p = p0 + li;
+    const bool valid = p < n;
+    const int64_t pc = valid ? p : n - 1;
+    const float *xrow = x + pc * C, *grow = gout + pc * C;
+    const int HM = H * M;
+
+    f32x4 O[CT];
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct) O[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int h = 0; h < H; ++h) {
+        f32x4 E[MT], Dz[MT];
+        logits_tile<C, M>(E, w2p, b2s, h, xrow, lane);
+        softmax_tile<MT>(E, valid);
+        dz_tile<C, M>(Dz, E, Z, dsr, dd, h, xrow, grow, inv_tau, lane);
+#pragma unroll
+        for (int km = 0; km < KM; ++km) {
+            Frag<float> wf, zf;
+            pack_b<MT>(E, km, wf);
+            pack_b<MT>(Dz, km, zf);
+#pragma unroll
+            for (int ct = 0; ct < CT; ++ct) {
+                const int c = ct * 16 + li;
+                Frag<float> a;
+                frag_slices<M>(a, W2 + (size_t)c * HM + h * M, km, g);
+                mma(O[ct], a, zf);
+                frag_slices<M>(a, dsT + ((size_t)h * C + c) * M, km, g);
+                mma(O[ct], a, wf);
+            }
+        }
+    }
+    if (valid)
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct)
+            *reinterpret_cast<float4 *>(dx + p * C + ct * 16 + g * 4) = float4{O[ct][0], O[ct][1], O[ct][2], O[ct][3]};
+}
+
+// Token side of the backward, one workgroup per head (256 threads):
+//   Z[h] = s1[h] W3_h            -> ds1, dW3_h
+//   s1 = softmax(q k^T / sqrt(dh)) v, q,k,v = s Wq,Wk,Wv  -> ds, dWq, dWk, dWv
+//   s = mean W1_h + b1_h          -> dmean, dW1_h, db1_h
+//   mean = s_raw / (d + eps) (0 where d + eps <= 0) -> ds_raw, dsT, dd
+// and db3 = sum_m dZ[0][m] (every head's weights sum to one per point).
+// Dynamic LDS: floats mean, dZ [M][C] and s, s1, q, k, v, ds1, dq, dk, dv, ds
+// [M][dh] and P, dP [M][M].
+__global__ __launch_bounds__(256, 1) void k_bw_token(
+    const float *__restrict__ s_raw, const float *__restrict__ dsum, const float *__restrict__ s,
+    const float *__restrict__ s1, const float *__restrict__ dZ, const float *__restrict__ W1,
+    const float *__restrict__ Wq, const float *__restrict__ Wk, const float *__restrict__ Wv,
+    const float *__restrict__ W3, int C, int H, int M, int dh, float eps, float *__restrict__ dsr,
+    float *__restrict__ dsT, float *__restrict__ dd, float *__restrict__ dW1, float *__restrict__ db1,
+    float *__restrict__ dWq, float *__restrict__ dWk, float *__restrict__ dWv, float *__restrict__ dW3,
+    float *__restrict__ db3) {
+    extern __shared__ float sm[];
+    const int h = blockIdx.x, tid = threadIdx.x, nt = blockDim.x;
+    const int HD = H * dh;
+    float *mean = sm, *gz = mean + M * C;
+    float *ss = gz + M * C, *s1s = ss + M * dh, *q = s1s + M * dh, *k = q + M * dh, *v = k + M * dh;
+    float *ds1 = v + M * dh, *dq = ds1 + M * dh, *dk = dq + M * dh, *dv = dk + M * dh, *ds = dv + M * dh;
+    float *P = ds + M * dh, *dP = P + M * M;
+    const float scale = 1.f / sqrtf((float)dh);
+    for (int i = tid; i < M * C; i += nt) {
+        const int m = i / C;
+        const float den = dsum[h * M + m] + eps;
+        mean[i] = den > 0.f ? s_raw[(size_t)h * M * C + i] / den : 0.f;
+        gz[i] = dZ[(size_t)h * M * C + i];
+    }
+    for (int i = tid; i < M * dh; i += nt) {
+        ss[i] = s[(size_t)h * M * dh + i];
+        s1s[i] = s1[(size_t)h * M * dh + i];
+    }
+    __syncthreads();
+    // ds1 = dZ W3_h^T; dW3_h = s1^T dZ; q, k, v
+    for (int i = tid; i < M * dh; i += nt) {
+        const int m = i / dh, j = i % dh;
+        float a = 0.f, aq = 0.f, ak = 0.f, av = 0.f;
+        for (int c = 0; c < C; ++c) a += gz[m * C + c] * W3[(size_t)(h * dh + j) * C + c];
+        for (int t = 0; t < dh; ++t) {
+            const float sv = ss[m * dh + t];
+            aq += sv * Wq[((size_t)h * dh + t) * dh + j];
+            ak += sv * Wk[((size_t)h * dh + t) * dh + j];
+            av += sv * Wv[((size_t)h * dh + t) * dh + j];
+        }
+        ds1[i] = a;
+        q[i] = aq;
+        k[i] = ak;
+        v[i] = av;
+    }
+    for (int i = tid; i < dh * C; i += nt) {
+        const int j = i / C, c = i % C;
+        float a = 0.f;
+        for (int m = 0; m < M; ++m) a += s1s[m * dh + j] * gz[m * C + c];
+        dW3[(size_t)(h * dh + j) * C + c] = a;
+    }
+    if (h == 0)
+        for (int c = tid; c < C; c += nt) {
+            float a = 0.f;
+            for (int m = 0; m < M; ++m) a += gz[m * C + c];
+            db3[c] = a;
+        }
+    __syncthreads();
+    // P = softmax_rows(q k^T * scale); dP = ds1 v^T
+    for (int i = tid; i < M * M; i += nt) {
+        const int a_ = i / M, b_ = i % M;
+        float dot = 0.f, dpv = 0.f;
+        for (int j = 0; j < dh; ++j) {
+            dot += q[a_ * dh + j] * k[b_ * dh + j];
+            dpv += ds1[a_ * dh + j] * v[b_ * dh + j];
+        }
+        P[i] = dot * scale;
+        dP[i] = dpv;
+    }
+    __syncthreads();
+    for (int a_ = tid; a_ < M; a_ += nt) {
+        float mx = P[a_ * M];
+        for (int b_ = 1; b_ < M; ++b_) mx = fmaxf(mx, P[a_ * M + b_]);
+        float sum = 0.f;
+        for (int b_ = 0; b_ < M; ++b_) {
+            const float e = expf(P[a_ * M + b_] - mx);
+            P[a_ * M + b_] = e;
+            sum += e;
+        }
+        const float inv = 1.f / sum;
+        float dot = 0.f;
+        for (int b_ = 0; b_ < M; ++b_) {
+            P[a_ * M + b_] *= inv;
+            dot += dP[a_ * M + b_] * P[a_ * M + b_];
+        }
+        // dP becomes da = P (dP - rowsum(dP P))
+        for (int b_ = 0; b_ < M; ++b_) dP[a_ * M + b_] = P[a_ * M + b_] * (dP[a_ * M + b_] - dot);
+    }
+    __syncthreads();
+    // dv = P^T ds1; dq = da k * scale; dk = da^T q * scale
+    for (int i = tid; i < M * dh; i += nt) {
+        const int m = i / dh, j = i % dh;
+        float av = 0.f, aq = 0.f, ak = 0.f;
+        for (int t = 0; t < M; ++t) {
+            av += P[t * M + m] * ds1[t * dh + j];
+            aq += dP[m * M + t] * k[t * dh + j];
+            ak += dP[t * M + m] * q[t * dh + j];
+        }
+        dv[i] = av;
+        dq[i] = aq * scale;
+        dk[i] = ak * scale;
+    }
+    __syncthreads();
+    // dWq/dWk/dWv = s^T (dq, dk, dv); ds = dq Wq^T + dk Wk^T + dv Wv^T
+    for (int i = tid; i < dh * dh; i += nt) {
+        const int t = i / dh, j = i % dh;
+        float aq = 0.f, ak = 0.f, av = 0.f;
+        for (int m = 0; m < M; ++m) {
+            const float sv = ss[m * dh + t];
+            aq += sv * dq[m * dh + j];
+            ak += sv * dk[m * dh + j];
+            av += sv * dv[m * dh + j];
+        }
+        dWq[(size_t)h * dh * dh + i] = aq;
+        dWk[(size_t)h * dh * dh + i] = ak;
+        dWv[(size_t)h * dh * dh + i] = av;
+    }
+    for (int i = tid; i < M * dh; i += nt) {
+        const int m = i / dh, t = i % dh;
+        float a = 0.f;
+        for (int j = 0; j < dh; ++j)
+            a += dq[m * dh + j] * Wq[((size_t)h * dh + t) * dh + j] + dk[m * dh + j] * Wk[((size_t)h * dh + t) * dh + j] +
+                 dv[m * dh + j] * Wv[((size_t)h * dh + t) * dh + j];
+        ds[i] = a;
+    }
+    __syncthreads();
+    // dW1_h = mean^T ds; db1_h = sum_m ds
+    for (int i = tid; i < C * dh; i += nt) {
+        const int c = i / dh, j = i % dh;
+        float a = 0.f;
+        for (int m = 0; m < M; ++m) a += mean[m * C + c] * ds[m * dh + j];
+        dW1[(size_t)c * HD + h * dh + j] = a;
+    }
+    for (int j = tid; j < dh; j += nt) {
+        float a = 0.f;
+        for (int m = 0; m < M; ++m) a += ds[m * dh + j];
+        db1[h * dh + j] = a;
+    }
+    // dmean = ds W1_h^T (kept in gz); ds_raw = dmean / den; dd = -sum_c dmean mean / den
+    for (int i = tid; i < M * C; i += nt) {
+        const int m = i / C, c = i % C;
+        float a = 0.f;
+        for (int j = 0; j < dh; ++j) a += ds[m * dh + j] * W1[(size_t)c * HD + h * dh + j];
+        const float den = dsum[h * M + m] + eps;
+        const float r = den > 0.f ? a / den : 0.f;
+        gz[i] = a;
+        dsr[(size_t)h * M * C + i] = r;
+        dsT[((size_t)h * C + c) * M + m] = r;
+    }
+    __syncthreads();
+    for (int m = tid; m < M; m += nt) {
+        const float den = dsum[h * M + m] + eps;
+        float a = 0.f;
+        for (int c = 0; c < C; ++c) a += gz[m * C + c] * mean[m * C + c];
+        dd[h * M + m] = den > 0.f ? -a / den : 0.f;
+    }
+}
+
+// dW2[c][h*M + m] = dW2T[h][m][c].
+__global__ void k_bw_transpose_w2(const float *__restrict__ dW2T, int C, int HM, float *__restrict__ dW2) {
+    const int64_t total = (int64_t)C * HM;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t c = i / HM, hm = i % HM;
+        dW2[i] = dW2T[hm * C + c];
+    }
+}
+
+}  // namespace ts3

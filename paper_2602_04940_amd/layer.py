@@ -121,6 +121,26 @@ class PhysicsAttention:
                                           _stream()), "ts3_layer_forward")
         return out
 
+    def backward(self, w: LayerWeights, x, g, tile: int, dx=None):
+        """Gradients of sum(g * x_out) after forward(w, x, ...) on this state:
+        returns (dx, {dW2, db2, dW1, db1, dWq, dWk, dWv, dW3, db3}) as device
+        float32 tensors shaped like x and the weights."""
+        self._check_x(x)
+        self._check_x(g, "g")
+        if dx is None:
+            dx = torch.empty_like(x)
+        self._check_x(dx, "dx")
+        grads = {}
+        for n in L.GRAD_NAMES:
+            wt = w.t[n[1:]]
+            shape = wt.shape if wt is not None else {"db2": (self.H * self.M,), "db1": (self.H * self.dh,),
+                                                     "db3": (self.C,)}[n]
+            grads[n] = torch.empty(shape, device=x.device, dtype=torch.float32)
+        gs = L.Grads(**{n: grads[n].data_ptr() for n in L.GRAD_NAMES})
+        L.check(L.lib().ts3_layer_backward(self.h, w.ref(), _ptr(x), _ptr(g), x.shape[0], tile, _ptr(dx),
+                                           ct.byref(gs), _stream()), "ts3_layer_backward")
+        return dx, grads
+
     def get(self, which: int) -> np.ndarray:
         H, M, C, dh = self.H, self.M, self.C, self.dh
         shape = {L.TS3_S_RAW: (H, M, C), L.TS3_D: (H, M), L.TS3_S: (H, M, dh), L.TS3_S1: (H, M, dh),

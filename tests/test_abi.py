@@ -33,6 +33,7 @@ def test_struct_layouts_match_header():
     assert ct.sizeof(L.Desc) == 48
     assert L.Desc.group_span.offset == 32 and L.Desc.max_points.offset == 40
     assert ct.sizeof(L.Weights) == 9 * ct.sizeof(ct.c_void_p)
+    assert ct.sizeof(L.Grads) == 9 * ct.sizeof(ct.c_void_p)
 
 
 def _desc(**kw):
