@@ -10,6 +10,11 @@ covers exactly --steps steps between synchronised HIP events.  The line also
 carries the dominant kernel's roofline figures (HIP-event launch durations on
 the launch stream) and the float64 oracle's throughput on host cores over a
 bounded sample.  Prints one JSON line on stdout; progress goes to stderr.
+
+--backward times a float32 training step of the layer instead (forward, then
+the backward with the slice weights recomputed per tile) on 2M volume points
+(C=128, H=8, M=64, 1M-point tiles), with the backward's roofline against the
+float32 matrix peak and the float64 backward oracle as the CPU baseline.
 """
 import argparse
 import hashlib
@@ -137,6 +142,114 @@ def cpu_baseline(x_dev, W, wl, sample):
                       f"points of the mesh: {dt:.1f} s"}
 
 
+METRIC_BW = "mesh points/s per Physics-Attention layer fwd+bwd @2M pts C=128 fp32; % roofline"
+PEAK_FP32_TFLOPS = 157.3    # MI355X dense float32 matrix peak
+
+
+def cpu_baseline_backward(x_dev, g_dev, W, wl, sample):
+    """The float64 oracle (as written): forward state and backward on the first
+    `sample` points, host cores."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import backward as BW
+    xs = x_dev[:sample].double().cpu().numpy()
+    gs = g_dev[:sample].double().cpu().numpy()
+    W64 = {k: np.asarray(v, np.float64) for k, v in W.items()}
+    t0 = time.perf_counter()
+    BW.layer_backward(xs, W64, gs, wl.H, wl.M, 1.0 / wl.tau, tile=wl.tile)
+    dt = time.perf_counter() - t0
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    return {"value": sample / dt, "unit": "points/s", "cores": threads, "kind": "oracle",
+            "sample": f"layer forward state + backward (all gradients) in float64 numpy on the first {sample} "
+                      f"points of the mesh: {dt:.1f} s"}
+
+
+def bench_backward(args):
+    """A training step of one layer in float32: the forward over the resident
+    points (which leaves the state the backward needs), then the backward with
+    the slice weights recomputed tile by tile."""
+    import torch
+
+    from paper_2602_04940_amd import LayerWeights, PhysicsAttention
+    from ts3_synth import WORKLOADS, make_weights
+    from ts3_synth.device_gen import DeviceVolume
+
+    wl = WORKLOADS["volume_2m_fp32"]
+    N = args.points or wl.N
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    log(f"generating {N} volume points on the device (C={wl.C}, fp32) and an output gradient")
+    x = torch.empty((N, wl.C), device=dev, dtype=torch.float32)
+    DeviceVolume(wl.seed, wl.C, dev, dtype=torch.float32).fill(x)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(wl.seed + 1000)
+    g = torch.randn((N, wl.C), device=dev, dtype=torch.float32, generator=gen)
+    out = torch.empty_like(x)
+    dx = torch.empty_like(x)
+    W = make_weights(wl.C, wl.H, wl.M, wl.dh, seed=0)
+    lw = LayerWeights(W, dev)
+    layer = PhysicsAttention(wl.C, wl.H, wl.M, wl.dh, wl.tau, "fp32", group_span=wl.group_span, max_points=N)
+    torch.cuda.synchronize()
+
+    def step():
+        layer.forward(lw, x, tile=wl.tile, chunk=wl.chunk, out=out)
+        return layer.backward(lw, x, g, tile=wl.tile, dx=dx)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"warmup {args.warmup} done; timing {args.steps} steps")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / max(args.steps, 1)
+
+    # forward and backward separately, on the launch stream
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    reps = max(args.steps, 1)
+    t_fw = t_bw = 0.0
+    for _ in range(reps):
+        ev[0].record()
+        layer.forward(lw, x, tile=wl.tile, chunk=wl.chunk, out=out)
+        ev[1].record()
+        layer.backward(lw, x, g, tile=wl.tile, dx=dx)
+        ev[2].record()
+        torch.cuda.synchronize()
+        t_fw += ev[0].elapsed_time(ev[1]) / reps
+        t_bw += ev[1].elapsed_time(ev[2]) / reps
+    log(f"{ms:.3f} ms/step: forward {t_fw:.3f} ms, backward {t_bw:.3f} ms")
+
+    # algorithmic backward flops per point: logits recomputed (2), w^T g (2),
+    # g.Z and x.ds_raw (4), x^T dz (2), dz W2^T (2), w ds_raw (2), each x C*H*M
+    flop_bw = 14 * wl.C * wl.H * wl.M
+    achieved = flop_bw * N / (t_bw * 1e-3) / 1e12
+    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_FP32_TFLOPS, 4), "traffic": None,
+                "kernel": "ts3_layer_backward (all launches)", "launch_ms": round(t_bw, 4), "launches": 1}
+    result = {
+        "metric": METRIC_BW, "value": N / (ms * 1e-3), "unit": "points/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic: seeded volume mesh (box minus car-like body), Fourier features, device-generated; "
+                "output gradient N(0,1)",
+        "config": {"workload": wl.name, "N": N, "C": wl.C, "H": wl.H, "M": wl.M, "dh": wl.dh, "tau": wl.tau,
+                   "tile": wl.tile, "chunk": wl.chunk, "group_span": wl.group_span},
+        "passes_ms": {"forward": round(t_fw, 3), "backward": round(t_bw, 3)},
+        "roofline": roofline,
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        sample = min(args.cpu_sample_backward, N)
+        log(f"timing the float64 backward oracle on {sample} points (host cores)")
+        result["cpu_baseline"] = cpu_baseline_backward(x, g, W, wl, sample)
+    layer.close()
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -149,6 +262,9 @@ def main():
     ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="write profiles/traffic.json from two --pmc runs of --pmc-driver")
     ap.add_argument("--command", default="", help="command line recorded with --summarize-traffic")
+    ap.add_argument("--backward", action="store_true",
+                    help="time a float32 training step (forward + backward) on 2M points instead")
+    ap.add_argument("--cpu-sample-backward", type=int, default=100_000)
     args = ap.parse_args()
     if args.summarize_traffic:
         summarize_traffic(*args.summarize_traffic, args.command)
@@ -161,6 +277,9 @@ def main():
               "(the layer shards by points with one all-gather of span partials; not built here)",
               file=sys.stderr)
         sys.exit(2)
+    if args.backward:
+        bench_backward(args)
+        return
 
     import numpy as np
     import torch

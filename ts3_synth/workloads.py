@@ -43,6 +43,11 @@ WORKLOADS = {
     # one layer of an 8-block stack on a 10M-point car surface (per-layer shape)
     "car_10m_bf16": Workload("car_10m_bf16", "car_surface", 3, 10_000_000, 256, 8, 64, 32, 0.5,
                              "bf16", 1_000_000, 1_000_000, 31_250),
+    # a training step of one layer (forward and backward, float32) on 2M volume
+    # points: a uniform sample of the volume mesh (its points are i.i.d.
+    # uniform in the domain, so the first 2M points are such a sample)
+    "volume_2m_fp32": Workload("volume_2m_fp32", "volume", 5, 2_000_000, 128, 8, 64, 16, 0.5,
+                               "fp32", 1_000_000, 1_000_000, 15_625),
     # cached-state inference over 100M volume points, 1M-point tiles and chunks
     "volume_100m_bf16": Workload("volume_100m_bf16", "volume", 4, 100_000_000, 128, 8, 64, 16, 0.5,
                                  "bf16", 1_000_000, 1_000_000, 15_625),
