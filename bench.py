@@ -265,6 +265,8 @@ def main():
     ap.add_argument("--backward", action="store_true",
                     help="time a float32 training step (forward + backward) on 2M points instead")
     ap.add_argument("--cpu-sample-backward", type=int, default=100_000)
+    ap.add_argument("--accum", choices=("fp32", "fp64"), default="fp32",
+                    help="precision of the fold of span partials (float64: Appendix A.4 robustness)")
     args = ap.parse_args()
     if args.summarize_traffic:
         summarize_traffic(*args.summarize_traffic, args.command)
@@ -303,7 +305,8 @@ def main():
 
     W = make_weights(wl.C, wl.H, wl.M, wl.dh, seed=0)
     lw = LayerWeights(W, dev)
-    layer = PhysicsAttention(wl.C, wl.H, wl.M, wl.dh, wl.tau, "bf16", group_span=wl.group_span, max_points=N)
+    layer = PhysicsAttention(wl.C, wl.H, wl.M, wl.dh, wl.tau, "bf16", group_span=wl.group_span, max_points=N,
+                             accum=args.accum)
     free, total = torch.cuda.mem_get_info()
     hbm_used_gb = (total - free) / 1e9
 
@@ -359,7 +362,7 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic: seeded volume mesh (box minus car-like body), Fourier features, device-generated",
         "config": {"workload": wl.name, "N": N, "C": wl.C, "H": wl.H, "M": wl.M, "dh": wl.dh, "tau": wl.tau,
-                   "tile": wl.tile, "chunk": wl.chunk, "group_span": wl.group_span,
+                   "tile": wl.tile, "chunk": wl.chunk, "group_span": wl.group_span, "accum": args.accum,
                    "hbm_used_gb": round(hbm_used_gb, 2), "state_bytes": layer.bytes()},
         "passes_ms": {"pass1": round(t_p1, 3), "state": round(t_mid, 3), "pass2": round(t_p2, 3)},
         "roofline": roofline,

@@ -49,6 +49,9 @@ typedef enum {
 
 typedef enum { TS3_FP32 = 0, TS3_BF16 = 1 } ts3_dtype;
 
+/* Precision of the fold of span partials (ts3_desc.accum). */
+typedef enum { TS3_ACCUM_FP32 = 0, TS3_ACCUM_FP64 = 1 } ts3_accum;
+
 /* Layer shape and numerics.
  *  C, H, M, dh : channels, heads, slices per head, head width; H*dh == C.
  *                Supported: (C, M) in {(64,16), (64,32), (128,16), (128,32),
@@ -64,6 +67,12 @@ typedef enum { TS3_FP32 = 0, TS3_BF16 = 1 } ts3_dtype;
  *  group_span  : Q, points per accumulation span (1 <= Q <= 2^30).  Pass 1
  *                reduces each span to one partial and sums spans in index
  *                order, so results do not depend on how the mesh is tiled.
+ *  accum       : ts3_accum, the precision of the fold of span partials (the
+ *                sum over tiles of Eq. (4); Appendix A.4 on accumulating over
+ *                very large meshes).  TS3_ACCUM_FP32 adds the float32 span
+ *                partials in float32; TS3_ACCUM_FP64 adds them in float64 and
+ *                rounds once to float32.  Each span's own partial is float32
+ *                either way.  Any other value is TS3_ERR_INVALID_ARG.
  *  max_points  : largest point index + 1 the state will accumulate; sizes the
  *                span partials (ceil(max_points / Q) * H * M * (C+1) floats). */
 typedef struct {
@@ -71,7 +80,7 @@ typedef struct {
     float temperature;
     float eps;
     int32_t io_dtype;
-    int32_t reserved;
+    int32_t accum;
     int64_t group_span;
     int64_t max_points;
 } ts3_desc;

@@ -15,10 +15,13 @@ TS3_FP32, TS3_BF16 = 0, 1
 TS3_S_RAW, TS3_D, TS3_S, TS3_S1, TS3_ZP = range(5)
 
 
+TS3_ACCUM_FP32, TS3_ACCUM_FP64 = 0, 1
+
+
 class Desc(ct.Structure):
     _fields_ = [("C", ct.c_int32), ("H", ct.c_int32), ("M", ct.c_int32), ("dh", ct.c_int32),
                 ("temperature", ct.c_float), ("eps", ct.c_float), ("io_dtype", ct.c_int32),
-                ("reserved", ct.c_int32), ("group_span", ct.c_int64), ("max_points", ct.c_int64)]
+                ("accum", ct.c_int32), ("group_span", ct.c_int64), ("max_points", ct.c_int64)]
 
 
 class Weights(ct.Structure):

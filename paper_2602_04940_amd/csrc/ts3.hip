@@ -226,6 +226,8 @@ ts3_status check_desc(const ts3_desc *d) {
         return fail(TS3_ERR_UNSUPPORTED, "H*dh (%d*%d) must equal C (%d)", d->H, d->dh, d->C);
     if (d->io_dtype != TS3_FP32 && d->io_dtype != TS3_BF16)
         return fail(TS3_ERR_INVALID_ARG, "io_dtype %d is not TS3_FP32 or TS3_BF16", d->io_dtype);
+    if (d->accum != TS3_ACCUM_FP32 && d->accum != TS3_ACCUM_FP64)
+        return fail(TS3_ERR_INVALID_ARG, "accum %d is not TS3_ACCUM_FP32 or TS3_ACCUM_FP64", d->accum);
     if (!(d->temperature > 0.f)) return fail(TS3_ERR_INVALID_ARG, "temperature must be > 0");
     if (!(d->eps >= 0.f) || std::isinf(d->eps)) return fail(TS3_ERR_INVALID_ARG, "eps must be finite and >= 0");
     if (d->group_span <= 0 || d->group_span > (1 << 30))
@@ -353,7 +355,7 @@ ts3_status ts3_state_create(const ts3_desc *desc, ts3_state **out) {
         int64_t bytes;
     } reqs[] = {
         {(void **)&st->partials, st->nspan_max * st->E * 4},
-        {(void **)&st->runs, st->nrun_max * st->E * 4},
+        {(void **)&st->runs, st->nrun_max * st->E * 8},  // float or double run sums
         {(void **)&st->s_raw, HM * d.C * 4},
         {(void **)&st->dsum, HM * 4},
         {(void **)&st->s, HM * d.dh * 4},
@@ -453,6 +455,34 @@ ts3_status ts3_slice_accumulate(ts3_state *st, const ts3_weights *w, const void 
     return TS3_OK;
 }
 
+}  // extern "C"
+
+namespace {
+
+// Ordered fold of the first nspan span partials into main [H*M*C] and the
+// column C entries into col [H*M] (the forward's fold kernels).
+template <typename T>
+ts3_status fold_partials_t(ts3_state *st, int64_t nspan, float *main, float *col, hipStream_t hs) {
+    const int64_t E = st->E;
+    const int64_t nrun = (nspan + FOLD - 1) / FOLD;
+    const unsigned gx = (unsigned)((E + 255) / 256);
+    T *runs = reinterpret_cast<T *>(st->runs);
+    hipLaunchKernelGGL(k_fold_runs<T>, dim3(gx, (unsigned)nrun), dim3(256), 0, hs, st->partials, E, nspan, runs);
+    LAUNCH_CHECK("fold_runs");
+    hipLaunchKernelGGL(k_fold_final<T>, dim3(gx), dim3(256), 0, hs, runs, E, nrun, st->desc.C, main, col);
+    LAUNCH_CHECK("fold_final");
+    return TS3_OK;
+}
+
+ts3_status fold_partials(ts3_state *st, int64_t nspan, float *main, float *col, hipStream_t hs) {
+    return st->desc.accum == TS3_ACCUM_FP64 ? fold_partials_t<double>(st, nspan, main, col, hs)
+                                            : fold_partials_t<float>(st, nspan, main, col, hs);
+}
+
+}  // namespace
+
+extern "C" {
+
 ts3_status ts3_slice_finalize(ts3_state *st, const ts3_weights *w, void *stream) {
     if (!st) return fail(TS3_ERR_INVALID_ARG, "state is NULL");
     if (!w || !w->W1) return fail(TS3_ERR_INVALID_ARG, "weights or W1 is NULL");
@@ -473,12 +503,8 @@ ts3_status ts3_slice_finalize(ts3_state *st, const ts3_weights *w, void *stream)
         LAUNCH_CHECK("zero spans");
         i = j;
     }
-    const int64_t nrun = (nspan + FOLD - 1) / FOLD;
-    const unsigned gx = (unsigned)((E + 255) / 256);
-    hipLaunchKernelGGL(k_fold_runs, dim3(gx, (unsigned)nrun), dim3(256), 0, hs, st->partials, E, nspan, st->runs);
-    LAUNCH_CHECK("fold_runs");
-    hipLaunchKernelGGL(k_fold_final, dim3(gx), dim3(256), 0, hs, st->runs, E, nrun, d.C, st->s_raw, st->dsum);
-    LAUNCH_CHECK("fold_final");
+    const ts3_status s = fold_partials(st, nspan, st->s_raw, st->dsum, hs);
+    if (s != TS3_OK) return s;
     const size_t lds = (size_t)d.M * d.C * 4;
     hipLaunchKernelGGL(k_finalize, dim3(d.H), dim3(256), lds, hs, st->s_raw, st->dsum, w->W1, w->b1, d.C, d.H,
                        d.M, d.dh, d.eps, st->s);
@@ -588,22 +614,6 @@ ts3_status ts3_layer_forward(ts3_state *st, const ts3_weights *w, const void *x,
     return s;
 }
 
-namespace {
-
-// Ordered fold of the first nspan span partials into main [H*M*C] and the
-// column C entries into col [H*M] (the forward's fold kernels).
-ts3_status fold_partials(ts3_state *st, int64_t nspan, float *main, float *col, hipStream_t hs) {
-    const int64_t E = st->E;
-    const int64_t nrun = (nspan + FOLD - 1) / FOLD;
-    const unsigned gx = (unsigned)((E + 255) / 256);
-    hipLaunchKernelGGL(k_fold_runs, dim3(gx, (unsigned)nrun), dim3(256), 0, hs, st->partials, E, nspan, st->runs);
-    LAUNCH_CHECK("fold_runs");
-    hipLaunchKernelGGL(k_fold_final, dim3(gx), dim3(256), 0, hs, st->runs, E, nrun, st->desc.C, main, col);
-    LAUNCH_CHECK("fold_final");
-    return TS3_OK;
-}
-
-}  // namespace
 
 ts3_status ts3_layer_backward(ts3_state *st, const ts3_weights *w, const void *x, const void *g, int64_t N,
                               int64_t tile, void *dx, const ts3_grads *gr, void *stream) {

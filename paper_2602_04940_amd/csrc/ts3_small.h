@@ -69,30 +69,33 @@ __global__ void k_zero(float *__restrict__ p, int64_t n) {
 // [H][M][C+1] is summed over spans 0..nspan-1 in two fixed levels (runs of
 // FOLD spans, then the runs in order), giving the same bits for any tiling.
 constexpr int FOLD = 64;
-__global__ void k_fold_runs(const float *__restrict__ partials, int64_t E, int64_t nspan,
-                            float *__restrict__ runs) {
+// T is the fold's accumulator: float, or double (the partials are added in
+// float64 and rounded once at the end); runs hold T.
+template <typename T>
+__global__ void k_fold_runs(const float *__restrict__ partials, int64_t E, int64_t nspan, T *__restrict__ runs) {
     const int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
     const int64_t run = blockIdx.y;
     if (e >= E) return;
     const int64_t s0 = run * FOLD;
     const int64_t s1 = s0 + FOLD < nspan ? s0 + FOLD : nspan;
-    float acc = 0.f;
-    for (int64_t s = s0; s < s1; ++s) acc += partials[s * E + e];
+    T acc = 0;
+    for (int64_t s = s0; s < s1; ++s) acc += (T)partials[s * E + e];
     runs[run * E + e] = acc;
 }
 
-__global__ void k_fold_final(const float *__restrict__ runs, int64_t E, int64_t nrun, int C,
-                             float *__restrict__ s_raw, float *__restrict__ dsum) {
+template <typename T>
+__global__ void k_fold_final(const T *__restrict__ runs, int64_t E, int64_t nrun, int C, float *__restrict__ s_raw,
+                             float *__restrict__ dsum) {
     const int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
     if (e >= E) return;
-    float acc = 0.f;
+    T acc = 0;
     for (int64_t r = 0; r < nrun; ++r) acc += runs[r * E + e];
     const int64_t hm = e / (C + 1);
     const int c = (int)(e - hm * (C + 1));
     if (c < C)
-        s_raw[hm * C + c] = acc;
+        s_raw[hm * C + c] = (float)acc;
     else
-        dsum[hm] = acc;
+        dsum[hm] = (float)acc;
 }
 
 // s[h][m][j] = (d^-1 s_raw)[h][m][:] . W1[:, h*dh + j] + b1[h*dh + j]; one

@@ -48,13 +48,14 @@ class PhysicsAttention:
     """A layer state: pass 1 accumulation, token-side work, pass 2 decoding."""
 
     def __init__(self, C, H, M, dh=None, temperature=0.5, dtype="bf16", group_span=32768,
-                 max_points=1 << 20, eps=0.0):
+                 max_points=1 << 20, eps=0.0, accum="fp32"):
         self.C, self.H, self.M = C, H, M
         self.dh = C // H if dh is None else dh
         self.dtype_name = dtype
         code, self.torch_dtype = _DTYPES[dtype]
+        acc = {"fp32": L.TS3_ACCUM_FP32, "fp64": L.TS3_ACCUM_FP64}[accum]
         self.desc = L.Desc(C=C, H=H, M=M, dh=self.dh, temperature=temperature, eps=eps, io_dtype=code,
-                           reserved=0, group_span=group_span, max_points=max_points)
+                           accum=acc, group_span=group_span, max_points=max_points)
         h = ct.c_void_p()
         L.check(L.lib().ts3_state_create(ct.byref(self.desc), ct.byref(h)), "ts3_state_create")
         self.h = h

@@ -37,7 +37,7 @@ def test_struct_layouts_match_header():
 
 
 def _desc(**kw):
-    d = dict(C=128, H=8, M=64, dh=16, temperature=0.5, eps=0.0, io_dtype=L.TS3_BF16, reserved=0,
+    d = dict(C=128, H=8, M=64, dh=16, temperature=0.5, eps=0.0, io_dtype=L.TS3_BF16, accum=L.TS3_ACCUM_FP32,
              group_span=1024, max_points=4096)
     d.update(kw)
     return L.Desc(**d)
@@ -49,6 +49,8 @@ def _desc(**kw):
     (dict(C=96, H=6), L.TS3_ERR_UNSUPPORTED),     # no kernel for C=96
     (dict(M=48), L.TS3_ERR_UNSUPPORTED),
     (dict(io_dtype=7), L.TS3_ERR_INVALID_ARG),
+    (dict(accum=2), L.TS3_ERR_INVALID_ARG),
+    (dict(accum=-1), L.TS3_ERR_INVALID_ARG),
     (dict(temperature=0.0), L.TS3_ERR_INVALID_ARG),
     (dict(temperature=float("nan")), L.TS3_ERR_INVALID_ARG),
     (dict(eps=-1.0), L.TS3_ERR_INVALID_ARG),
