@@ -55,8 +55,9 @@ typedef enum { TS3_ACCUM_FP32 = 0, TS3_ACCUM_FP64 = 1 } ts3_accum;
 /* Layer shape and numerics.
  *  C, H, M, dh : channels, heads, slices per head, head width; H*dh == C.
  *                Supported: (C, M) in {(64,16), (64,32), (128,16), (128,32),
- *                (128,64)} with (5*M*dh + M*M) * 4 bytes <= 160 KiB (the
- *                token-attention working set); otherwise TS3_ERR_UNSUPPORTED.
+ *                (128,64)}, and (256,64) with bf16 storage, with
+ *                (5*M*dh + M*M) * 4 bytes <= 160 KiB (the token-attention
+ *                working set); otherwise TS3_ERR_UNSUPPORTED.
  *  temperature : tau > 0 of the slice softmax; +inf gives uniform weights.
  *  eps         : added to d before the division in finalize (the paper uses 0).
  *                A slice with d + eps <= 0 has a zero mean state.

@@ -15,6 +15,7 @@
 #include "ts3_pass1.h"
 #include "ts3_pass1w8.h"
 #include "ts3_pass1pc.h"
+#include "ts3_pass1wide.h"
 #include "ts3_backward.h"
 #include "ts3_pass2.h"
 #include "ts3_small.h"
@@ -72,7 +73,12 @@ struct Kernels {
 template <typename T, int C, int M>
 void launch_pass1(const void *x, int64_t n, int64_t span0, int32_t Q, int32_t nspan, int32_t H,
                   const void *w2p, const float *b2s, float *partials, hipStream_t st) {
-    if constexpr (sizeof(T) == 2 && M >= 32 && C == 128) {
+    if constexpr (sizeof(T) == 2 && C == 256) {
+        // Wide rows: channels split over the waves; XCD groups of 8 spans.
+        const int groups = (nspan + 7) / 8;
+        hipLaunchKernelGGL((k_slice_accumulate_wide<C, M>), dim3(groups * 8 * H), dim3(256), 0, st,
+                           (const bf16_t *)x, n, span0, Q, nspan, H, (const bf16_t *)w2p, b2s, partials);
+    } else if constexpr (sizeof(T) == 2 && M >= 32 && C == 128) {
         // Two heads per workgroup whenever H is even (independently of the
         // span count, so that every tiling sums a span the same way).
         if (H % 2 == 0)
@@ -103,7 +109,7 @@ hipError_t launch_pass2(const void *x, int64_t n, int32_t H, const void *w2p, co
                         const void *zp, void *out, hipStream_t st) {
     using Cfg = Pass2Cfg<T, C, M>;
     const int64_t nblk = (n + Cfg::POINTS_PER_WG - 1) / Cfg::POINTS_PER_WG;
-    if constexpr (sizeof(T) == 2) {
+    if constexpr (sizeof(T) == 2 && C <= 128) {
         using WCfg = Pass2W8Cfg<T, C, M>;
         const size_t lds = WCfg::lds_bytes(H);
         static size_t static_lds = SIZE_MAX;
@@ -164,7 +170,9 @@ void launch_bw_dx(const float *x, const float *g, int64_t n, int32_t H, const fl
 }
 
 template <typename T, int C, int M> Kernels make_kernels() {
-    if constexpr (sizeof(T) == 4)
+    if constexpr (C > 128 && sizeof(T) == 4)
+        return Kernels{nullptr, nullptr, nullptr, nullptr};  // float32 rows of 1 KB: no pass-1 kernel
+    else if constexpr (sizeof(T) == 4)
         return Kernels{&launch_pass1<T, C, M>, &launch_pass2<T, C, M>, &launch_bw_head<C, M>, &launch_bw_dx<C, M>};
     else
         return Kernels{&launch_pass1<T, C, M>, &launch_pass2<T, C, M>, nullptr, nullptr};
@@ -174,13 +182,14 @@ bool find_kernels(int dtype, int C, int M, Kernels *k) {
 #define TS3_SHAPE(CC, MM)                                                                      \
     if (C == CC && M == MM) {                                                                  \
         *k = dtype == TS3_BF16 ? make_kernels<bf16_t, CC, MM>() : make_kernels<float, CC, MM>(); \
-        return true;                                                                           \
+        return k->pass1 != nullptr;                                                            \
     }
     TS3_SHAPE(64, 16)
     TS3_SHAPE(64, 32)
     TS3_SHAPE(128, 16)
     TS3_SHAPE(128, 32)
     TS3_SHAPE(128, 64)
+    TS3_SHAPE(256, 64)
 #undef TS3_SHAPE
     return false;
 }
@@ -238,7 +247,7 @@ ts3_status check_desc(const ts3_desc *d) {
     Kernels k;
     if (!find_kernels(d->io_dtype, d->C, d->M, &k))
         return fail(TS3_ERR_UNSUPPORTED, "no kernel for C=%d, M=%d (supported: C in {64,128} with "
-                    "M in {16,32}, or C=128 with M=64)", d->C, d->M);
+                    "M in {16,32}, C=128 with M=64, or C=256 with M=64 in bf16)", d->C, d->M);
     if ((5 * d->M * d->dh + d->M * d->M) * 4 > ATTN_LDS_MAX)
         return fail(TS3_ERR_UNSUPPORTED, "token attention needs (5*M*dh + M*M) floats <= 160 KiB of LDS");
     const int64_t nspan = (d->max_points + d->group_span - 1) / d->group_span;

@@ -48,6 +48,7 @@ def _desc(**kw):
     (dict(H=4), L.TS3_ERR_UNSUPPORTED),           # H*dh != C
     (dict(C=96, H=6), L.TS3_ERR_UNSUPPORTED),     # no kernel for C=96
     (dict(M=48), L.TS3_ERR_UNSUPPORTED),
+    (dict(C=256, H=8, dh=32, io_dtype=L.TS3_FP32), L.TS3_ERR_UNSUPPORTED),  # wide rows are bf16 only
     (dict(io_dtype=7), L.TS3_ERR_INVALID_ARG),
     (dict(accum=2), L.TS3_ERR_INVALID_ARG),
     (dict(accum=-1), L.TS3_ERR_INVALID_ARG),

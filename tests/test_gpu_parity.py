@@ -127,6 +127,29 @@ def test_shapes_ragged_tiles_random_biases(C, H, M, dtype):
             assert rel_l2(st[k], ref_st[k]) <= BF16_TOL, k
 
 
+@pytest.mark.parametrize("C,H,M", [(256, 8, 64), (256, 4, 64)])
+def test_wide_rows_bf16_ragged_spans_random_biases(C, H, M):
+    """C = 256 (the car-surface stack's width): the channel-split pass 1 with
+    128-point super-blocks; spans of 3 super-blocks, the last span and the
+    last super-block ragged."""
+    N, Q, tile, chunk = 2000, 384, 768, 333
+    banner(f"wide shape C={C} H={H} M={M} bf16 N={N} tile={tile} Q={Q}")
+    from ts3_synth import round_bf16
+    rng = np.random.default_rng(C * 1000 + H * 10 + M)
+    x = round_bf16(rng.standard_normal((N, C)))
+    W = make_weights(C, H, M, C // H, seed=3, bias_seed=4)
+    got, st, _ = _run(x, W, C, H, M, "bf16", 0.5, tile, chunk, Q)
+    ref = oracle.layer_forward_fast(x, W, H, M, 2.0)
+    ref_st = oracle.build_state(x, W, H, M, 2.0)
+    assert rel_l2(got, ref) <= BF16_TOL
+    for k in ("s_raw", "d", "Z"):
+        assert rel_l2(st[k], ref_st[k]) <= BF16_TOL, k
+    got1, st1, _ = _run(x, W, C, H, M, "bf16", 0.5, 2304, N, Q)
+    assert np.array_equal(got1, got)
+    for k in ("s_raw", "d", "Z"):
+        assert np.array_equal(st1[k], st[k]), k
+
+
 @pytest.mark.parametrize("Q", [96, 100])
 def test_bf16_two_head_workgroups_odd_block_counts(Q):
     """Pass 1 with two heads per workgroup: a span of Q = 96 points has three
