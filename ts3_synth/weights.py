@@ -39,3 +39,25 @@ def make_weights(C: int, H: int, M: int, dh: int, seed: int = 0, bias_seed: int 
         w["b3"] = rb.uniform(-0.1, 0.1, C)
     # stored as float32; the float64 views below hold exactly the stored values
     return {k: np.ascontiguousarray(v, dtype=np.float32) for k, v in w.items()}
+
+
+def make_block_weights(C: int, H: int, M: int, dh: int, F: int, seed: int = 0, bias_seed: int | None = None):
+    """Weights of one pre-norm Transolver block: the Physics-Attention weights of
+    ``make_weights(seed, bias_seed)`` plus LayerNorm affines ln1_g, ln1_b,
+    ln2_g, ln2_b [C] and the feed-forward W_a [C, F], b_a [F], W_b [F, C],
+    b_b [C].  W_a, W_b are Xavier-uniform from ``default_rng(seed + 7919)``;
+    without ``bias_seed`` the gammas are one and the betas and biases zero,
+    with it they are 1 + U(-0.1, 0.1) and U(-0.1, 0.1)."""
+    w = make_weights(C, H, M, dh, seed, bias_seed)
+    rng = np.random.default_rng(seed + 7919)
+    w["Wa"] = xavier_uniform(rng, (C, F), C, F)
+    w["Wb"] = xavier_uniform(rng, (F, C), F, C)
+    if bias_seed is None:
+        w["ln1_g"], w["ln2_g"] = np.ones(C), np.ones(C)
+        w["ln1_b"], w["ln2_b"], w["ba"], w["bb"] = np.zeros(C), np.zeros(C), np.zeros(F), np.zeros(C)
+    else:
+        rb = np.random.default_rng(bias_seed + 7919)
+        w["ln1_g"], w["ln1_b"] = 1.0 + rb.uniform(-0.1, 0.1, C), rb.uniform(-0.1, 0.1, C)
+        w["ln2_g"], w["ln2_b"] = 1.0 + rb.uniform(-0.1, 0.1, C), rb.uniform(-0.1, 0.1, C)
+        w["ba"], w["bb"] = rb.uniform(-0.1, 0.1, F), rb.uniform(-0.1, 0.1, C)
+    return {k: np.ascontiguousarray(v, dtype=np.float32) for k, v in w.items()}
