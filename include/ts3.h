@@ -200,6 +200,57 @@ ts3_status ts3_state_get(const ts3_state *st, int32_t which, float *host_dst, in
 ts3_status ts3_state_set(ts3_state *st, const ts3_weights *w, int32_t which,
                          const float *host_src, int64_t n, const float *host_b3, void *stream);
 
+/* ------------------------------------------------------------------------
+ * Transolver block stack (the model around the layer: section 3 and the
+ * 8-layer configuration of Table 7).  Each block is pre-norm with residuals,
+ * a form the paper does not spell out and that is taken from the Transolver
+ * family:
+ *     y   = x + PA(LN1(x))
+ *     out = y + W_b^T GELU(W_a^T LN2(y) + b_a) + b_b
+ * LayerNorm over the C channels with affine gamma/beta and eps 1e-5 (biased
+ * variance); GELU in its exact form x * Phi(x) (erf evaluated to 1.5e-7).
+ * Activations are bf16 [N][C]; the feed-forward products run on bf16 matrix
+ * cores with float32 accumulation; each block keeps its own layer state, so
+ * every block's physical state Z stays cached (section 3.3). */
+typedef struct {
+    ts3_weights pa;               /* Physics-Attention weights (as above) */
+    const float *ln1_g, *ln1_b;   /* [C] LayerNorm before the attention */
+    const float *ln2_g, *ln2_b;   /* [C] LayerNorm before the feed-forward */
+    const float *Wa, *ba;         /* [C, F], [F]: first feed-forward map */
+    const float *Wb, *bb;         /* [F, C], [C]: second feed-forward map */
+} ts3_block_weights;               /* device float32; no pointer may be NULL
+                                      except the pa biases */
+
+typedef struct ts3_stack ts3_stack; /* opaque */
+
+/* A stack of n_blocks blocks of layer shape `desc` (bf16 storage) with hidden
+ * width `hidden` = F.  Supported (C, F): (128, 512), (256, 1024); otherwise
+ * TS3_ERR_UNSUPPORTED.  Allocates n_blocks layer states plus two activation
+ * buffers of max_points * C bf16 and one block's feed-forward fragments. */
+ts3_status ts3_stack_create(const ts3_desc *desc, int32_t n_blocks, int32_t hidden, ts3_stack **out);
+ts3_status ts3_stack_free(ts3_stack *s);
+ts3_status ts3_stack_bytes(const ts3_stack *s, int64_t *bytes);
+
+/* Block l's layer state (owned by the stack; valid until ts3_stack_free),
+ * for ts3_state_get / ts3_state_set. */
+ts3_status ts3_stack_layer(ts3_stack *s, int32_t l, ts3_state **layer);
+
+/* The whole stack over a resident mesh x (bf16 [N][C], overwritten with the
+ * last block's output): per block, ts3_layer_forward with `tile` and `chunk`
+ * on LN1(x), then the feed-forward half.  blocks[0..n_blocks-1].  Leaves
+ * every block's state ATTENDED (its cached Z).  Allocates nothing. */
+ts3_status ts3_stack_forward(ts3_stack *s, const ts3_block_weights *blocks, void *x, int64_t N,
+                             int64_t tile, int64_t chunk, void *stream);
+
+/* Decoding at arbitrary query points from the cached states (section 3.3,
+ * Eq. (5)): q (bf16 [n][C], overwritten) runs through every block with its
+ * Physics-Attention decoded from that block's Z (ts3_deslice in chunks of
+ * `chunk` points) instead of re-slicing the mesh.  Every block's state must
+ * be ATTENDED (after ts3_stack_forward, or ts3_state_set on each layer).
+ * n <= max_points; n == 0 is a no-op. */
+ts3_status ts3_stack_decode(ts3_stack *s, const ts3_block_weights *blocks, void *q, int64_t n, int64_t chunk,
+                            void *stream);
+
 const char *ts3_status_string(ts3_status s);
 const char *ts3_last_error(void); /* thread-local detail of the last failure */
 

@@ -37,6 +37,12 @@ class Grads(ct.Structure):
 
 GRAD_NAMES = [n for n, _ in Grads._fields_]
 
+BLOCK_EXTRA_NAMES = ("ln1_g", "ln1_b", "ln2_g", "ln2_b", "Wa", "ba", "Wb", "bb")
+
+
+class BlockWeights(ct.Structure):
+    _fields_ = [("pa", Weights)] + [(n, ct.c_void_p) for n in BLOCK_EXTRA_NAMES]
+
 _P = ct.c_void_p
 # name -> (restype, argtypes); must match include/ts3.h
 SIGNATURES = {
@@ -53,6 +59,12 @@ SIGNATURES = {
                                       ct.POINTER(Grads), _P]),
     "ts3_state_get": (ct.c_int, [_P, ct.c_int32, _P, ct.c_int64, _P]),
     "ts3_state_set": (ct.c_int, [_P, ct.POINTER(Weights), ct.c_int32, _P, ct.c_int64, _P, _P]),
+    "ts3_stack_create": (ct.c_int, [ct.POINTER(Desc), ct.c_int32, ct.c_int32, ct.POINTER(_P)]),
+    "ts3_stack_free": (ct.c_int, [_P]),
+    "ts3_stack_bytes": (ct.c_int, [_P, ct.POINTER(ct.c_int64)]),
+    "ts3_stack_layer": (ct.c_int, [_P, ct.c_int32, ct.POINTER(_P)]),
+    "ts3_stack_forward": (ct.c_int, [_P, ct.POINTER(BlockWeights), _P, ct.c_int64, ct.c_int64, ct.c_int64, _P]),
+    "ts3_stack_decode": (ct.c_int, [_P, ct.POINTER(BlockWeights), _P, ct.c_int64, ct.c_int64, _P]),
     "ts3_status_string": (ct.c_char_p, [ct.c_int]),
     "ts3_last_error": (ct.c_char_p, []),
 }

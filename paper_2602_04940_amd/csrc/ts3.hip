@@ -740,3 +740,5 @@ ts3_status ts3_state_set(ts3_state *st, const ts3_weights *w, int32_t which, con
 }
 
 }  // extern "C"
+
+#include "ts3_stack.h"

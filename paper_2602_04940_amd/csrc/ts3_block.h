@@ -1,0 +1,327 @@
+// Kernels of the pre-norm Transolver block around the Physics-Attention layer
+// (the model context of section 3; 8 blocks in the paper's Table 7):
+//
+//   y   = x + PA(LN1(x))
+//   out = y + W_b^T GELU(W_a^T LN2(y) + b_a) + b_b
+//
+// bf16 activations [N][C] between kernels, float32 arithmetic inside, bf16
+// matrix-core operands with float32 accumulation.
+//
+//   k_layernorm     LN1 of the first block (later blocks get theirs from the
+//                   previous block's feed-forward epilogue).
+//   k_prep_mlp      W_a and W_b as bf16 matrix-core fragments, chunked by 64
+//                   hidden units: [F/64][W_a^T part | W_b part], 64*C elements
+//                   each, so one linear copy stages a chunk.
+//   k_mlp_residual  one kernel for the rest of the block: y = x + PA output,
+//                   LN2, both feed-forward products with the exact GELU between
+//                   them, the residual, and optionally the next block's LN1.
+//
+// k_mlp_residual: four waves per workgroup, 32 points per wave (two 16-point
+// tiles).  Each wave keeps LN2(y) of its points as B fragments (K = channels)
+// in registers and the 16 x C output accumulator out^T[c][p]; the hidden layer
+// is walked in 64-unit chunks staged in LDS (two slots, one chunk ahead):
+//   GEMM1  H^T[f][p] = W_a^T[f][:] . LN2(y)[p][:] + b_a[f]   (A = staged W_a^T)
+//   GELU   in registers; the 16 x 4 outputs of two hidden tiles are exactly a
+//          B fragment of the second product (K slot (g, t) <-> hidden unit
+//          32km + 16(t>>2) + 4g + (t&3)), so h never leaves registers;
+//   GEMM2  out^T[c][p] += W_b^T[c][:] . h[p][:]                (A = staged W_b)
+// Output rows of W_b's fragments follow zchan(), so a lane ends up holding the
+// eight consecutive channels 32k + 8g .. +7 of its point: the same channels
+// it loaded, which keeps the residual and the next LayerNorm in registers.
+#pragma once
+#include "ts3_device.h"
+#include "ts3_pass2.h"  // zchan
+
+namespace ts3 {
+
+constexpr float BLOCK_LN_EPS = 1e-5f;
+
+// erf by Abramowitz & Stegun, Handbook of Mathematical Functions, formula
+// 7.1.26 (|error| <= 1.5e-7; the hidden activations are stored as bf16).
+__device__ __forceinline__ float erf_as(float x) {
+    const float a = fabsf(x);
+    const float t = __builtin_amdgcn_rcpf(1.f + 0.3275911f * a);
+    const float poly = t * (0.254829592f + t * (-0.284496736f + t * (1.421413741f + t * (-1.453152027f +
+                                                                                           t * 1.061405429f))));
+    const float e = 1.f - poly * __builtin_amdgcn_exp2f(-a * a * 1.4426950408889634f);
+    return copysignf(e, x);
+}
+__device__ __forceinline__ float gelu_exact(float x) { return 0.5f * x * (1.f + erf_as(x * 0.70710678118654752f)); }
+
+__device__ __forceinline__ void unpack8(const uint4 &u, float (&v)[8]) {
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        v[2 * i] = __uint_as_float(w[i] << 16);
+        v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+    }
+}
+__device__ __forceinline__ uint4 pack8(const float (&v)[8]) {
+    typedef __attribute__((ext_vector_type(8))) __bf16 b8;
+    b8 b;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) b[i] = (__bf16)v[i];
+    return __builtin_bit_cast(uint4, b);
+}
+
+// LayerNorm over C channels of bf16 rows; C/8 lanes per row, 8 channels each.
+template <int C>
+__global__ __launch_bounds__(256) void k_layernorm(const bf16_t *__restrict__ x, int64_t n,
+                                                   const float *__restrict__ gam, const float *__restrict__ bet,
+                                                   bf16_t *__restrict__ out) {
+    constexpr int LPR = C / 8, RPW = 64 / LPR;
+    const int lane = threadIdx.x & 63, sub = lane / LPR, cl = lane % LPR;
+    const int64_t waves = (int64_t)gridDim.x * (blockDim.x >> 6);
+    float gv[8], bv[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        gv[i] = gam[8 * cl + i];
+        bv[i] = bet[8 * cl + i];
+    }
+    for (int64_t r0 = ((int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6)) * RPW; r0 < n;
+         r0 += waves * RPW) {
+        const int64_t row = r0 + sub;
+        const int64_t rc = row < n ? row : n - 1;
+        float v[8];
+        unpack8(*reinterpret_cast<const uint4 *>(x + rc * C + 8 * cl), v);
+        float s = 0.f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) s += v[i];
+#pragma unroll
+        for (int m = 1; m < LPR; m <<= 1) s += __shfl_xor(s, m);
+        const float mean = s * (1.f / C);
+        float q = 0.f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            v[i] -= mean;
+            q += v[i] * v[i];
+        }
+#pragma unroll
+        for (int m = 1; m < LPR; m <<= 1) q += __shfl_xor(q, m);
+        const float rstd = 1.f / sqrtf(q * (1.f / C) + BLOCK_LN_EPS);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = v[i] * rstd * gv[i] + bv[i];
+        if (row < n) *reinterpret_cast<uint4 *>(out + row * C + 8 * cl) = pack8(v);
+    }
+}
+
+template <int C> struct MlpCfg {
+    static constexpr int FC = 64, HT = FC / 16, KM = FC / 32, CK = C / 32, CT = C / 16;
+    static constexpr int PART = 64 * C;                 // elements of each half of a chunk
+    static constexpr int CHUNK_BYTES = 2 * PART * 2;    // bf16
+    static constexpr int COPIES = CHUNK_BYTES / 1024;   // 1 KB wave copies per chunk
+    static constexpr int WAVES = 4;
+    static_assert(COPIES % WAVES == 0, "copies split evenly over the waves");
+};
+
+// Fragments of chunk j (hidden units 64j .. 64j+63):
+//   W_a^T part, index ((ht*CK + kc)*64 + l)*8 + t:
+//       W_a[c = 32kc + 8(l>>4) + t][f = 64j + 16ht + (l&15)]
+//   W_b part,   index ((ct*KM + km)*64 + l)*8 + t:
+//       W_b[f = 64j + 32km + 16(t>>2) + 4(l>>4) + (t&3)][c = zchan(ct, l&15)]
+template <int C>
+__global__ void k_prep_mlp(const float *__restrict__ Wa, const float *__restrict__ Wb, int F,
+                           bf16_t *__restrict__ frag) {
+    using Cfg = MlpCfg<C>;
+    const int64_t total = (int64_t)(F / Cfg::FC) * 2 * Cfg::PART;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t j = i / (2 * Cfg::PART);
+        const int e = (int)(i % (2 * Cfg::PART));
+        const int t = e & 7, l = (e >> 3) & 63, r = e >> 9;
+        float v;
+        if (e < Cfg::PART) {
+            const int kc = r % Cfg::CK, ht = r / Cfg::CK;
+            const int c = 32 * kc + 8 * (l >> 4) + t;
+            const int64_t f = 64 * j + 16 * ht + (l & 15);
+            v = Wa[(int64_t)c * F + f];
+        } else {
+            const int r2 = r - Cfg::PART / 512;
+            const int km = r2 % Cfg::KM, ct = r2 / Cfg::KM;
+            const int64_t f = 64 * j + 32 * km + 16 * (t >> 2) + 4 * (l >> 4) + (t & 3);
+            const int c = zchan(ct, l & 15);
+            v = Wb[f * C + c];
+        }
+        frag[i].bits = __builtin_bit_cast(uint16_t, (__bf16)v);
+    }
+}
+
+// x, pa  : [n][C] bf16, the block input and its Physics-Attention output
+// ln2_*  : LN2 affine [C]; frag: k_prep_mlp output; ba [F], bb [C]
+// lnn_*  : the next block's LN1 affine, or NULL (then xn is not written)
+// xo     : [n][C] bf16 block output (may alias x); xn: LN1 of xo for the next
+//          block (may alias nothing that is read here)
+// grid   : ceil(n / 128) workgroups of 256 threads
+template <int C, int F>
+__global__ __launch_bounds__(256, 1) void k_mlp_residual(
+    const bf16_t *x, const bf16_t *__restrict__ pa, int64_t n, const float *__restrict__ ln2_g,
+    const float *__restrict__ ln2_b, const bf16_t *__restrict__ frag, const float *__restrict__ ba,
+    const float *__restrict__ bb, const float *__restrict__ lnn_g, const float *__restrict__ lnn_b, bf16_t *xo,
+    bf16_t *__restrict__ xn) {
+    using Cfg = MlpCfg<C>;
+    constexpr int CK = Cfg::CK, CT = Cfg::CT, HT = Cfg::HT, KM = Cfg::KM, NCHUNK = F / Cfg::FC;
+    constexpr int CB = Cfg::CHUNK_BYTES, WA_BYTES = Cfg::PART * 2;
+    static_assert(F % Cfg::FC == 0, "hidden width in 64-unit chunks");
+    __shared__ __attribute__((aligned(1024))) unsigned char lds[2 * CB];
+
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+    const int li = lane & 15, g = lane >> 4;
+    const int64_t p0 = ((int64_t)blockIdx.x * Cfg::WAVES + wave) * 32;
+
+    // Stage chunk j into slot sl (linear: the fragments are stored in order).
+    auto issue = [&](int j, int sl) {
+        const unsigned char *src = reinterpret_cast<const unsigned char *>(frag) + (size_t)j * CB;
+        const uint32_t base = lds_addr(lds) + sl * CB;
+#pragma unroll
+        for (int c = 0; c < Cfg::COPIES / Cfg::WAVES; ++c) {
+            const int k = wave * (Cfg::COPIES / Cfg::WAVES) + c;
+            dma16(src + k * 1024 + lane * 16, base + k * 1024);
+        }
+    };
+    issue(0, 0);
+
+    // y = x + pa and LN2(y) as B fragments: tile pt, lane (li, g) holds point
+    // p0 + 16pt + li, channels 32k + 8g .. +7 in slot t of fragment k.
+    Frag<bf16_t> yb[2][CK];
+#pragma unroll
+    for (int pt = 0; pt < 2; ++pt) {
+        int64_t p = p0 + 16 * pt + li;
+        p = p < n ? p : n - 1;
+        float y[CK][8];
+        float s = 0.f;
+#pragma unroll
+        for (int k = 0; k < CK; ++k) {
+            float a[8], b[8];
+            unpack8(*reinterpret_cast<const uint4 *>(x + p * C + 32 * k + 8 * g), a);
+            unpack8(*reinterpret_cast<const uint4 *>(pa + p * C + 32 * k + 8 * g), b);
+#pragma unroll
+            for (int t = 0; t < 8; ++t) {
+                y[k][t] = a[t] + b[t];
+                s += y[k][t];
+            }
+        }
+        const float mean = xrow_sum(s) * (1.f / C);
+        float q = 0.f;
+#pragma unroll
+        for (int k = 0; k < CK; ++k)
+#pragma unroll
+            for (int t = 0; t < 8; ++t) {
+                y[k][t] -= mean;
+                q += y[k][t] * y[k][t];
+            }
+        const float rstd = 1.f / sqrtf(xrow_sum(q) * (1.f / C) + BLOCK_LN_EPS);
+#pragma unroll
+        for (int k = 0; k < CK; ++k) {
+            const float4 g0 = *reinterpret_cast<const float4 *>(ln2_g + 32 * k + 8 * g);
+            const float4 g1 = *reinterpret_cast<const float4 *>(ln2_g + 32 * k + 8 * g + 4);
+            const float4 b0 = *reinterpret_cast<const float4 *>(ln2_b + 32 * k + 8 * g);
+            const float4 b1 = *reinterpret_cast<const float4 *>(ln2_b + 32 * k + 8 * g + 4);
+            const float gg[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
+            const float bbv[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+#pragma unroll
+            for (int t = 0; t < 8; t += 2)
+                yb[pt][k].set2(t, y[k][t] * rstd * gg[t] + bbv[t], y[k][t + 1] * rstd * gg[t + 1] + bbv[t + 1]);
+        }
+    }
+
+    f32x4 Z[CT][2];
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct) Z[ct][0] = Z[ct][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    for (int j = 0; j < NCHUNK; ++j) {
+        const int sl = j & 1;
+        wait_vmcnt<0>();
+        __syncthreads();  // chunk j staged; every wave is done with chunk j-1's slot
+        if (j + 1 < NCHUNK) issue(j + 1, sl ^ 1);
+        const unsigned char *wa = lds + sl * CB, *wb = wa + WA_BYTES;
+        f32x4 Hh[HT][2];
+#pragma unroll
+        for (int ht = 0; ht < HT; ++ht) {
+            const float4 b = *reinterpret_cast<const float4 *>(ba + 64 * j + 16 * ht + 4 * g);
+            Hh[ht][0] = Hh[ht][1] = f32x4{b.x, b.y, b.z, b.w};
+        }
+#pragma unroll
+        for (int kc = 0; kc < CK; ++kc)
+#pragma unroll
+            for (int ht = 0; ht < HT; ++ht) {
+                Frag<bf16_t> a;
+                a.v = *reinterpret_cast<const bf16x8 *>(wa + ((ht * CK + kc) * 64 + lane) * 16);
+                mma(Hh[ht][0], a, yb[0][kc]);
+                mma(Hh[ht][1], a, yb[1][kc]);
+            }
+        Frag<bf16_t> hb[2][KM];
+#pragma unroll
+        for (int pt = 0; pt < 2; ++pt)
+#pragma unroll
+            for (int km = 0; km < KM; ++km)
+#pragma unroll
+                for (int t = 0; t < 8; t += 2) {
+                    const int ht = 2 * km + (t >> 2);
+                    hb[pt][km].set2(t, gelu_exact(Hh[ht][pt][t & 3]), gelu_exact(Hh[ht][pt][(t & 3) + 1]));
+                }
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+            for (int km = 0; km < KM; ++km) {
+                Frag<bf16_t> a;
+                a.v = *reinterpret_cast<const bf16x8 *>(wb + ((ct * KM + km) * 64 + lane) * 16);
+                mma(Z[ct][0], a, hb[0][km]);
+                mma(Z[ct][1], a, hb[1][km]);
+            }
+    }
+
+    // out = x + pa + z + bb; lane (li, g) of tile pt holds channels
+    // 32k + 8g + 4h + r in Z[2k + h][pt][r].
+#pragma unroll
+    for (int pt = 0; pt < 2; ++pt) {
+        const int64_t p = p0 + 16 * pt + li;
+        const int64_t pc = p < n ? p : n - 1;
+        float o[CK][8];
+        float s = 0.f;
+#pragma unroll
+        for (int k = 0; k < CK; ++k) {
+            float a[8], b[8];
+            unpack8(*reinterpret_cast<const uint4 *>(x + pc * C + 32 * k + 8 * g), a);
+            unpack8(*reinterpret_cast<const uint4 *>(pa + pc * C + 32 * k + 8 * g), b);
+            const float4 c0 = *reinterpret_cast<const float4 *>(bb + 32 * k + 8 * g);
+            const float4 c1 = *reinterpret_cast<const float4 *>(bb + 32 * k + 8 * g + 4);
+            const float cb[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+#pragma unroll
+            for (int t = 0; t < 8; ++t) {
+                o[k][t] = (a[t] + b[t]) + (Z[2 * k + (t >> 2)][pt][t & 3] + cb[t]);
+                s += o[k][t];
+            }
+        }
+        if (lnn_g) {  // uniform
+            // the next block's LN1 of the rounded output
+            float sr = 0.f;
+#pragma unroll
+            for (int k = 0; k < CK; ++k)
+#pragma unroll
+                for (int t = 0; t < 8; ++t) {
+                    o[k][t] = (float)(__bf16)o[k][t];
+                    sr += o[k][t];
+                }
+            const float mean = xrow_sum(sr) * (1.f / C);
+            float q = 0.f;
+#pragma unroll
+            for (int k = 0; k < CK; ++k)
+#pragma unroll
+                for (int t = 0; t < 8; ++t) q += (o[k][t] - mean) * (o[k][t] - mean);
+            const float rstd = 1.f / sqrtf(xrow_sum(q) * (1.f / C) + BLOCK_LN_EPS);
+#pragma unroll
+            for (int k = 0; k < CK; ++k) {
+                float v[8];
+#pragma unroll
+                for (int t = 0; t < 8; ++t) v[t] = (o[k][t] - mean) * rstd * lnn_g[32 * k + 8 * g + t] + lnn_b[32 * k + 8 * g + t];
+                if (p < n) *reinterpret_cast<uint4 *>(xn + p * C + 32 * k + 8 * g) = pack8(v);
+            }
+        }
+        (void)s;
+        if (p < n)
+#pragma unroll
+            for (int k = 0; k < CK; ++k) *reinterpret_cast<uint4 *>(xo + p * C + 32 * k + 8 * g) = pack8(o[k]);
+    }
+}
+
+}  // namespace ts3

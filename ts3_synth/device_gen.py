@@ -73,3 +73,22 @@ class DeviceVolume:
             if progress and (k % 10 == 9 or k * G.CHUNK + n == N):
                 progress(k + 1)
         return x
+
+
+class DeviceSurface(DeviceVolume):
+    """Points on the car-like body's surface (uniform in direction, the host
+    recipe of ``geometry.car_surface_chunk``), features over the body's padded
+    bounding box; chunk k uses ``manual_seed(seed * 2**32 + k)``."""
+
+    def __init__(self, seed: int, C: int, device="cuda", dtype=torch.bfloat16):
+        super().__init__(seed, C, device, dtype)
+        lo, hi = G.CarBody().bbox()
+        self.lo = torch.tensor(lo, device=self.device, dtype=torch.float64)
+        self.hi = torch.tensor(hi, device=self.device, dtype=torch.float64)
+
+    def points(self, k: int, n: int = G.CHUNK):
+        gen = torch.Generator(device=self.device)
+        gen.manual_seed(self.seed * (1 << 32) + k)
+        g = torch.randn((n, 3), generator=gen, device=self.device, dtype=torch.float64)
+        u = g / g.norm(dim=1, keepdim=True)
+        return self.centre + self._radius(u)[:, None] * u
