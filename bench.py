@@ -15,6 +15,11 @@ bounded sample.  Prints one JSON line on stdout; progress goes to stderr.
 the backward with the slice weights recomputed per tile) on 2M volume points
 (C=128, H=8, M=64, 1M-point tiles), with the backward's roofline against the
 float32 matrix peak and the float64 backward oracle as the CPU baseline.
+
+--stack times the 8-block pre-norm Transolver stack (Physics-Attention plus a
+4C feed-forward network per block) on a 10M-point car surface (C=256, H=8,
+M=64, bf16), with the dominant kernel's roofline and the float64 block oracle
+as the CPU baseline.
 """
 import argparse
 import hashlib
@@ -250,6 +255,131 @@ def bench_backward(args):
     print(json.dumps(result), flush=True)
 
 
+METRIC_STACK = "mesh points/s through an 8-block Transolver stack fwd @10M pts C=256 bf16; % roofline"
+STACK_BLOCKS = 8
+
+
+def cpu_baseline_stack(x_dev, blocks, wl, sample):
+    """The float64 block oracle (as written) over the first `sample` points."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import block as BK
+    xs = x_dev[:sample].double().cpu().numpy()
+    b64 = [{k: np.asarray(v, np.float64) for k, v in b.items()} for b in blocks]
+    t0 = time.perf_counter()
+    BK.stack_forward(xs, b64, wl.H, wl.M, 1.0 / wl.tau)
+    dt = time.perf_counter() - t0
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    return {"value": sample / dt, "unit": "points/s", "cores": threads, "kind": "oracle",
+            "sample": f"{len(blocks)}-block stack forward in float64 numpy on the first {sample} points of the "
+                      f"mesh (as their own mesh): {dt:.1f} s"}
+
+
+def bench_stack(args):
+    """The 8-block pre-norm Transolver stack (Physics-Attention + 4C feed-forward
+    per block) over the 10M-point car surface, bf16 activations."""
+    import torch
+
+    from paper_2602_04940_amd import BlockWeights, PhysicsAttention, TransolverStack
+    from ts3_synth import WORKLOADS, make_block_weights
+    from ts3_synth.device_gen import DeviceSurface
+
+    wl = WORKLOADS["car_10m_bf16"]
+    N = args.points or wl.N
+    F = 4 * wl.C
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    log(f"generating {N} car-surface points on the device (C={wl.C}, bf16)")
+    x0 = torch.empty((N, wl.C), device=dev, dtype=torch.bfloat16)
+    DeviceSurface(wl.seed, wl.C, dev).fill(x0)
+    x = torch.empty_like(x0)
+    blocks = [make_block_weights(wl.C, wl.H, wl.M, wl.dh, F, seed=100 + l) for l in range(STACK_BLOCKS)]
+    dblocks = [BlockWeights(b, dev) for b in blocks]
+    stack = TransolverStack(wl.C, wl.H, wl.M, STACK_BLOCKS, F, wl.dh, wl.tau, group_span=wl.group_span,
+                            max_points=N)
+    torch.cuda.synchronize()
+
+    def step():
+        stack.forward(dblocks, x, tile=wl.tile, chunk=wl.chunk)
+
+    for _ in range(args.warmup):
+        x.copy_(x0)
+        step()
+    torch.cuda.synchronize()
+    log(f"warmup {args.warmup} done; timing {args.steps} steps (the input is restored between steps, untimed)")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    total = 0.0
+    for _ in range(args.steps):
+        x.copy_(x0)
+        torch.cuda.synchronize()
+        e0.record()
+        step()
+        e1.record()
+        torch.cuda.synchronize()
+        total += e0.elapsed_time(e1)
+    ms = total / max(args.steps, 1)
+    log(f"{ms:.3f} ms/step")
+    free, tot = torch.cuda.mem_get_info()
+
+    # Per-kernel launch durations on the launch stream: one block's
+    # Physics-Attention passes (a layer of the same shape) and its feed-forward.
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+    ntile, nchunk = -(-N // wl.tile), -(-N // wl.chunk)
+    lw = dblocks[0].pa
+    with PhysicsAttention(wl.C, wl.H, wl.M, wl.dh, wl.tau, "bf16", group_span=wl.group_span, max_points=N) as layer:
+        pa = torch.empty_like(x0)
+        layer.forward(lw, x0, tile=wl.tile, chunk=wl.chunk, out=pa)
+        torch.cuda.synchronize()
+        ev[0].record()
+        layer.reset()
+        for t in range(ntile):
+            layer.accumulate(lw, x0[t * wl.tile:(t + 1) * wl.tile], t * wl.tile)
+        ev[1].record()
+        layer.finalize(lw)
+        layer.attention(lw)
+        ev[2].record()
+        for c in range(nchunk):
+            layer.deslice(lw, x0[c * wl.chunk:(c + 1) * wl.chunk], pa[c * wl.chunk:(c + 1) * wl.chunk])
+        ev[3].record()
+        x.copy_(x0)
+        stack.feedforward(dblocks, 0, x, pa)
+        ev[4].record()
+        torch.cuda.synchronize()
+    t_p1, t_mid, t_p2, t_ff = (ev[i].elapsed_time(ev[i + 1]) for i in range(4))
+    log(f"per block: pass1 {t_p1:.3f} ms ({ntile} launches), state {t_mid:.3f} ms, pass2 {t_p2:.3f} ms "
+        f"({nchunk} launches), feed-forward {t_ff:.3f} ms (1 launch + fragment prep)")
+    pa_flop = 4 * wl.C * wl.H * wl.M          # per point and pass
+    ff_flop = 4 * wl.C * F                    # per point: two products of 2*C*F
+    cands = [("k_mlp_residual", t_ff, 1, ff_flop * N), ("k_slice_accumulate_wide", t_p1, ntile, pa_flop * N),
+             ("k_deslice", t_p2, nchunk, pa_flop * N)]
+    kname, t_all, nl, flop_all = max(cands, key=lambda c: c[1])
+    t_launch = t_all / nl
+    achieved = flop_all / nl / (t_launch * 1e-3) / 1e12
+    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None, "kernel": kname,
+                "launch_ms": round(t_launch, 4), "launches": nl}
+    result = {
+        "metric": METRIC_STACK, "value": N / (ms * 1e-3), "unit": "points/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic: seeded car-like surface mesh, Fourier features, device-generated; random-init blocks",
+        "config": {"workload": wl.name, "N": N, "C": wl.C, "H": wl.H, "M": wl.M, "dh": wl.dh, "tau": wl.tau,
+                   "blocks": STACK_BLOCKS, "hidden": F, "tile": wl.tile, "chunk": wl.chunk,
+                   "group_span": wl.group_span, "hbm_used_gb": round((tot - free) / 1e9, 2)},
+        "per_block_ms": {"pass1": round(t_p1, 3), "state": round(t_mid, 3), "pass2": round(t_p2, 3),
+                         "feedforward": round(t_ff, 3)},
+        "roofline": roofline,
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        sample = min(args.cpu_sample_stack, N)
+        log(f"timing the float64 stack oracle on {sample} points (host cores)")
+        result["cpu_baseline"] = cpu_baseline_stack(x0, blocks, wl, sample)
+    stack.close()
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -265,6 +395,9 @@ def main():
     ap.add_argument("--backward", action="store_true",
                     help="time a float32 training step (forward + backward) on 2M points instead")
     ap.add_argument("--cpu-sample-backward", type=int, default=100_000)
+    ap.add_argument("--stack", action="store_true",
+                    help="time the 8-block Transolver stack on the 10M-point car surface (C=256) instead")
+    ap.add_argument("--cpu-sample-stack", type=int, default=20_000)
     ap.add_argument("--accum", choices=("fp32", "fp64"), default="fp32",
                     help="precision of the fold of span partials (float64: Appendix A.4 robustness)")
     args = ap.parse_args()
@@ -281,6 +414,9 @@ def main():
         sys.exit(2)
     if args.backward:
         bench_backward(args)
+        return
+    if args.stack:
+        bench_stack(args)
         return
 
     import numpy as np

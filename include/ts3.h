@@ -251,6 +251,14 @@ ts3_status ts3_stack_forward(ts3_stack *s, const ts3_block_weights *blocks, void
 ts3_status ts3_stack_decode(ts3_stack *s, const ts3_block_weights *blocks, void *q, int64_t n, int64_t chunk,
                             void *stream);
 
+/* The feed-forward half of block l on its own: x (bf16 [n][C], overwritten)
+ * becomes y + W_b^T GELU(W_a^T LN2(y) + b_a) + b_b with y = x + pa, where pa
+ * is block l's Physics-Attention output for x.  If xn_next is not NULL and
+ * l + 1 < n_blocks, also writes block l+1's LN1 of the result there.  The
+ * block's own share of ts3_stack_forward; exposed for timing and tests. */
+ts3_status ts3_stack_feedforward(ts3_stack *s, const ts3_block_weights *blocks, int32_t l, void *x,
+                                 const void *pa, int64_t n, void *xn_next, void *stream);
+
 const char *ts3_status_string(ts3_status s);
 const char *ts3_last_error(void); /* thread-local detail of the last failure */
 

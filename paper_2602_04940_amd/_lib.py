@@ -65,6 +65,7 @@ SIGNATURES = {
     "ts3_stack_layer": (ct.c_int, [_P, ct.c_int32, ct.POINTER(_P)]),
     "ts3_stack_forward": (ct.c_int, [_P, ct.POINTER(BlockWeights), _P, ct.c_int64, ct.c_int64, ct.c_int64, _P]),
     "ts3_stack_decode": (ct.c_int, [_P, ct.POINTER(BlockWeights), _P, ct.c_int64, ct.c_int64, _P]),
+    "ts3_stack_feedforward": (ct.c_int, [_P, ct.POINTER(BlockWeights), ct.c_int32, _P, _P, ct.c_int64, _P, _P]),
     "ts3_status_string": (ct.c_char_p, [ct.c_int]),
     "ts3_last_error": (ct.c_char_p, []),
 }

@@ -193,4 +193,32 @@ ts3_status ts3_stack_decode(ts3_stack *s, const ts3_block_weights *blocks, void 
     });
 }
 
+ts3_status ts3_stack_feedforward(ts3_stack *s, const ts3_block_weights *blocks, int32_t l, void *x, const void *pa,
+                                 int64_t n, void *xn_next, void *stream) {
+    if (!s || !blocks) return fail(TS3_ERR_INVALID_ARG, "NULL argument");
+    if (l < 0 || l >= s->L) return fail(TS3_ERR_INVALID_ARG, "block %d of %d", l, s->L);
+    if (n < 0 || n > s->desc.max_points) return fail(TS3_ERR_INVALID_ARG, "0 <= n <= max_points required");
+    if (n == 0) return TS3_OK;
+    if (!x || !pa || ((uintptr_t)x & 15) || ((uintptr_t)pa & 15) || ((uintptr_t)xn_next & 15))
+        return fail(TS3_ERR_INVALID_ARG, "x, pa (and xn_next) must be 16-byte aligned device pointers");
+    ts3_status st = check_block(&blocks[l]);
+    if (st != TS3_OK) return st;
+    const bool next = xn_next && l + 1 < s->L;
+    if (next) {
+        st = check_block(&blocks[l + 1]);
+        if (st != TS3_OK) return st;
+    }
+    StackKernels k{};
+    find_stack_kernels(s->desc.C, s->F, &k);
+    hipStream_t hs = (hipStream_t)stream;
+    const ts3_block_weights &b = blocks[l];
+    k.prep(b.Wa, b.Wb, s->F, s->frag, hs);
+    LAUNCH_CHECK("feed-forward fragments");
+    k.mlp((const bf16_t *)x, (const bf16_t *)pa, n, b.ln2_g, b.ln2_b, s->frag, b.ba, b.bb,
+          next ? blocks[l + 1].ln1_g : nullptr, next ? blocks[l + 1].ln1_b : nullptr, (bf16_t *)x, (bf16_t *)xn_next,
+          hs);
+    LAUNCH_CHECK("feed-forward");
+    return TS3_OK;
+}
+
 }  // extern "C"

@@ -84,6 +84,17 @@ class TransolverStack:
         L.check(L.lib().ts3_stack_decode(self.h, arr, _ptr(q), q.shape[0], chunk, _stream()), "ts3_stack_decode")
         return q
 
+    def feedforward(self, blocks, l: int, x, pa, xn_next=None):
+        """Block l's feed-forward half in place on x given its attention output pa."""
+        self._check(x)
+        self._check(pa)
+        if xn_next is not None:
+            self._check(xn_next)
+        arr = self._blocks(blocks)
+        L.check(L.lib().ts3_stack_feedforward(self.h, arr, l, _ptr(x), _ptr(pa), x.shape[0], _ptr(xn_next),
+                                              _stream()), "ts3_stack_feedforward")
+        return x
+
     def layer(self, l: int) -> PhysicsAttention:
         """Block l's layer state as a (non-owning) PhysicsAttention view."""
         h = ct.c_void_p()
