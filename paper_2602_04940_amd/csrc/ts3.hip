@@ -18,6 +18,7 @@
 #include "ts3_pass1wide.h"
 #include "ts3_backward.h"
 #include "ts3_pass2.h"
+#include "ts3_pass2wide.h"
 #include "ts3_small.h"
 
 using namespace ts3;
@@ -109,7 +110,12 @@ hipError_t launch_pass2(const void *x, int64_t n, int32_t H, const void *w2p, co
                         const void *zp, void *out, hipStream_t st) {
     using Cfg = Pass2Cfg<T, C, M>;
     const int64_t nblk = (n + Cfg::POINTS_PER_WG - 1) / Cfg::POINTS_PER_WG;
-    if constexpr (sizeof(T) == 2 && C <= 128) {
+    if constexpr (sizeof(T) == 2 && C == 256) {
+        // Wide rows: heads streamed through LDS, 128 points per workgroup.
+        hipLaunchKernelGGL((k_deslice_wide<C, M>), dim3((unsigned)((n + 127) / 128)), dim3(256), 0, st,
+                           (const bf16_t *)x, n, H, (const bf16_t *)w2p, b2s, (const bf16_t *)zp, (bf16_t *)out);
+        return hipSuccess;
+    } else if constexpr (sizeof(T) == 2 && C <= 128) {
         using WCfg = Pass2W8Cfg<T, C, M>;
         const size_t lds = WCfg::lds_bytes(H);
         static size_t static_lds = SIZE_MAX;
