@@ -16,8 +16,9 @@
 //                   LN2, both feed-forward products with the exact GELU between
 //                   them, the residual, and optionally the next block's LN1.
 //
-// k_mlp_residual: four waves per workgroup, 32 points per wave (two 16-point
-// tiles).  Each wave keeps LN2(y) of its points as B fragments (K = channels)
+// k_mlp_residual: 128 points per workgroup, as eight waves of one 16-point
+// tile (the stack's choice: two waves per SIMD hide each other's GELU and
+// LDS latency) or four waves of two tiles.  Each wave keeps LN2(y) of its points as B fragments (K = channels)
 // in registers and the 16 x C output accumulator out^T[c][p]; the hidden layer
 // is walked in 64-unit chunks staged in LDS (two slots, one chunk ahead):
 //   GEMM1  H^T[f][p] = W_a^T[f][:] . LN2(y)[p][:] + b_a[f]   (A = staged W_a^T)
@@ -105,12 +106,12 @@ __global__ __launch_bounds__(256) void k_layernorm(const bf16_t *__restrict__ x,
     }
 }
 
-template <int C> struct MlpCfg {
+template <int C, int PT = 2> struct MlpCfg {
     static constexpr int FC = 64, HT = FC / 16, KM = FC / 32, CK = C / 32, CT = C / 16;
     static constexpr int PART = 64 * C;                 // elements of each half of a chunk
     static constexpr int CHUNK_BYTES = 2 * PART * 2;    // bf16
     static constexpr int COPIES = CHUNK_BYTES / 1024;   // 1 KB wave copies per chunk
-    static constexpr int WAVES = 4;
+    static constexpr int WAVES = 8 / PT;                // 128 points per workgroup
     static_assert(COPIES % WAVES == 0, "copies split evenly over the waves");
 };
 
@@ -150,14 +151,15 @@ __global__ void k_prep_mlp(const float *__restrict__ Wa, const float *__restrict
 // lnn_*  : the next block's LN1 affine, or NULL (then xn is not written)
 // xo     : [n][C] bf16 block output (may alias x); xn: LN1 of xo for the next
 //          block (may alias nothing that is read here)
-// grid   : ceil(n / 128) workgroups of 256 threads
-template <int C, int F>
-__global__ __launch_bounds__(256, 1) void k_mlp_residual(
+// PT     : 16-point tiles per wave (2: four waves; 1: eight waves, two per SIMD)
+// grid   : ceil(n / 128) workgroups of 512 / PT threads
+template <int C, int F, int PT>
+__global__ __launch_bounds__(512 / PT, 1) void k_mlp_residual(
     const bf16_t *x, const bf16_t *__restrict__ pa, int64_t n, const float *__restrict__ ln2_g,
     const float *__restrict__ ln2_b, const bf16_t *__restrict__ frag, const float *__restrict__ ba,
     const float *__restrict__ bb, const float *__restrict__ lnn_g, const float *__restrict__ lnn_b, bf16_t *xo,
     bf16_t *__restrict__ xn) {
-    using Cfg = MlpCfg<C>;
+    using Cfg = MlpCfg<C, PT>;
     constexpr int CK = Cfg::CK, CT = Cfg::CT, HT = Cfg::HT, KM = Cfg::KM, NCHUNK = F / Cfg::FC;
     constexpr int CB = Cfg::CHUNK_BYTES, WA_BYTES = Cfg::PART * 2;
     static_assert(F % Cfg::FC == 0, "hidden width in 64-unit chunks");
@@ -166,7 +168,7 @@ __global__ __launch_bounds__(256, 1) void k_mlp_residual(
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     const int li = lane & 15, g = lane >> 4;
-    const int64_t p0 = ((int64_t)blockIdx.x * Cfg::WAVES + wave) * 32;
+    const int64_t p0 = ((int64_t)blockIdx.x * Cfg::WAVES + wave) * (16 * PT);
 
     // Stage chunk j into slot sl (linear: the fragments are stored in order).
     auto issue = [&](int j, int sl) {
@@ -182,9 +184,9 @@ __global__ __launch_bounds__(256, 1) void k_mlp_residual(
 
     // y = x + pa and LN2(y) as B fragments: tile pt, lane (li, g) holds point
     // p0 + 16pt + li, channels 32k + 8g .. +7 in slot t of fragment k.
-    Frag<bf16_t> yb[2][CK];
+    Frag<bf16_t> yb[PT][CK];
 #pragma unroll
-    for (int pt = 0; pt < 2; ++pt) {
+    for (int pt = 0; pt < PT; ++pt) {
         int64_t p = p0 + 16 * pt + li;
         p = p < n ? p : n - 1;
         float y[CK][8];
@@ -224,9 +226,11 @@ __global__ __launch_bounds__(256, 1) void k_mlp_residual(
         }
     }
 
-    f32x4 Z[CT][2];
+    f32x4 Z[CT][PT];
 #pragma unroll
-    for (int ct = 0; ct < CT; ++ct) Z[ct][0] = Z[ct][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+        for (int pt = 0; pt < PT; ++pt) Z[ct][pt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     for (int j = 0; j < NCHUNK; ++j) {
         const int sl = j & 1;
@@ -234,11 +238,12 @@ __global__ __launch_bounds__(256, 1) void k_mlp_residual(
         __syncthreads();  // chunk j staged; every wave is done with chunk j-1's slot
         if (j + 1 < NCHUNK) issue(j + 1, sl ^ 1);
         const unsigned char *wa = lds + sl * CB, *wb = wa + WA_BYTES;
-        f32x4 Hh[HT][2];
+        f32x4 Hh[HT][PT];
 #pragma unroll
         for (int ht = 0; ht < HT; ++ht) {
             const float4 b = *reinterpret_cast<const float4 *>(ba + 64 * j + 16 * ht + 4 * g);
-            Hh[ht][0] = Hh[ht][1] = f32x4{b.x, b.y, b.z, b.w};
+#pragma unroll
+            for (int pt = 0; pt < PT; ++pt) Hh[ht][pt] = f32x4{b.x, b.y, b.z, b.w};
         }
 #pragma unroll
         for (int kc = 0; kc < CK; ++kc)
@@ -246,12 +251,12 @@ __global__ __launch_bounds__(256, 1) void k_mlp_residual(
             for (int ht = 0; ht < HT; ++ht) {
                 Frag<bf16_t> a;
                 a.v = *reinterpret_cast<const bf16x8 *>(wa + ((ht * CK + kc) * 64 + lane) * 16);
-                mma(Hh[ht][0], a, yb[0][kc]);
-                mma(Hh[ht][1], a, yb[1][kc]);
-            }
-        Frag<bf16_t> hb[2][KM];
 #pragma unroll
-        for (int pt = 0; pt < 2; ++pt)
+                for (int pt = 0; pt < PT; ++pt) mma(Hh[ht][pt], a, yb[pt][kc]);
+            }
+        Frag<bf16_t> hb[PT][KM];
+#pragma unroll
+        for (int pt = 0; pt < PT; ++pt)
 #pragma unroll
             for (int km = 0; km < KM; ++km)
 #pragma unroll
@@ -265,15 +270,15 @@ __global__ __launch_bounds__(256, 1) void k_mlp_residual(
             for (int km = 0; km < KM; ++km) {
                 Frag<bf16_t> a;
                 a.v = *reinterpret_cast<const bf16x8 *>(wb + ((ct * KM + km) * 64 + lane) * 16);
-                mma(Z[ct][0], a, hb[0][km]);
-                mma(Z[ct][1], a, hb[1][km]);
+#pragma unroll
+                for (int pt = 0; pt < PT; ++pt) mma(Z[ct][pt], a, hb[pt][km]);
             }
     }
 
     // out = x + pa + z + bb; lane (li, g) of tile pt holds channels
     // 32k + 8g + 4h + r in Z[2k + h][pt][r].
 #pragma unroll
-    for (int pt = 0; pt < 2; ++pt) {
+    for (int pt = 0; pt < PT; ++pt) {
         const int64_t p = p0 + 16 * pt + li;
         const int64_t pc = p < n ? p : n - 1;
         float o[CK][8];

@@ -3,8 +3,8 @@
 // Algorithm 1 deslice loop).
 //
 // At C = 256 one head's W2' and Z operands are 32 KB each, so the heads are
-// streamed through LDS: four waves per workgroup, 32 points per wave (two
-// 16-point tiles), head h's W2'^T and Z^T fragments staged in one of two LDS
+// streamed through LDS: 128 points per workgroup (eight waves of one 16-point
+// tile, or four of two), head h's W2'^T and Z^T fragments staged in one of two LDS
 // slots one head ahead of use (linear direct copies: the prepared arrays are
 // already in fragment order).  Per head and wave:
 //   logits  L[m][p] = W2'_h^T x_p + b2'   (A = staged W2'^T, B = x rows kept in
@@ -21,23 +21,24 @@
 
 namespace ts3 {
 
-template <int C, int M> struct Pass2WideCfg {
+template <int C, int M, int PT = 2> struct Pass2WideCfg {
     static constexpr int MT = M / 16, CK = C / 32, CT = C / 16, KM = M / 32;
     static constexpr int PART = M * C;                 // elements of W2'_h (= of Z_h)
     static constexpr int HEAD_BYTES = 2 * PART * 2;    // bf16 W2'_h then Z_h
     static constexpr int COPIES = HEAD_BYTES / 1024;
-    static constexpr int WAVES = 4;
+    static constexpr int WAVES = 8 / PT;               // 128 points per workgroup
     static_assert(M % 32 == 0, "slice tiles pair into K32 steps");
     static_assert(COPIES % (2 * WAVES) == 0, "copies split evenly over the waves and halves");
 };
 
 // x: [n][C] bf16; w2p: [H][MT][CK][64][8]; zp: [H][CT][KM][64][8];
-// b2s: [H*M]; out: [n][C] bf16.  Grid: ceil(n / 128) workgroups of 256 threads.
-template <int C, int M>
-__global__ __launch_bounds__(256, 1) void k_deslice_wide(const bf16_t *__restrict__ x, int64_t n, int32_t H,
+// b2s: [H*M]; out: [n][C] bf16.  PT: 16-point tiles per wave.  Grid:
+// ceil(n / 128) workgroups of 512 / PT threads.
+template <int C, int M, int PT>
+__global__ __launch_bounds__(512 / PT, 1) void k_deslice_wide(const bf16_t *__restrict__ x, int64_t n, int32_t H,
                                                           const bf16_t *__restrict__ w2p, const float *__restrict__ b2s,
                                                           const bf16_t *__restrict__ zp, bf16_t *__restrict__ out) {
-    using Cfg = Pass2WideCfg<C, M>;
+    using Cfg = Pass2WideCfg<C, M, PT>;
     constexpr int MT = Cfg::MT, CK = Cfg::CK, CT = Cfg::CT, KM = Cfg::KM;
     constexpr int HB = Cfg::HEAD_BYTES, PB = Cfg::PART * 2;
     __shared__ __attribute__((aligned(1024))) unsigned char lds[2 * HB];
@@ -45,7 +46,7 @@ __global__ __launch_bounds__(256, 1) void k_deslice_wide(const bf16_t *__restric
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     const int li = lane & 15, g = lane >> 4;
-    const int64_t p0 = ((int64_t)blockIdx.x * Cfg::WAVES + wave) * 32;
+    const int64_t p0 = ((int64_t)blockIdx.x * Cfg::WAVES + wave) * (16 * PT);
 
     // Head h's W2'^T then Z^T fragments into slot sl.
     auto issue = [&](int h, int sl) {
@@ -64,17 +65,19 @@ __global__ __launch_bounds__(256, 1) void k_deslice_wide(const bf16_t *__restric
 
     // x rows of the wave's points as logits B fragments: tile pt, lane (li, g)
     // holds channels 32k + 8g .. +7 of point p0 + 16pt + li in fragment k.
-    Frag<bf16_t> xb[2][CK];
+    Frag<bf16_t> xb[PT][CK];
 #pragma unroll
-    for (int pt = 0; pt < 2; ++pt) {
+    for (int pt = 0; pt < PT; ++pt) {
         int64_t p = p0 + 16 * pt + li;
         p = p < n ? p : n - 1;
 #pragma unroll
         for (int k = 0; k < CK; ++k) load8(xb[pt][k], x + p * C + 32 * k + 8 * g);
     }
-    f32x4 O[CT][2];
+    f32x4 O[CT][PT];
 #pragma unroll
-    for (int ct = 0; ct < CT; ++ct) O[ct][0] = O[ct][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+        for (int pt = 0; pt < PT; ++pt) O[ct][pt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     for (int h = 0; h < H; ++h) {
         const int sl = h & 1;
@@ -82,11 +85,12 @@ __global__ __launch_bounds__(256, 1) void k_deslice_wide(const bf16_t *__restric
         __syncthreads();  // head h staged; every wave is done with head h-1's slot
         if (h + 1 < H) issue(h + 1, sl ^ 1);
         const unsigned char *wa = lds + sl * HB, *za = wa + PB;
-        f32x4 L[MT][2];
+        f32x4 L[MT][PT];
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
             const float4 b = *reinterpret_cast<const float4 *>(b2s + h * M + 16 * mt + 4 * g);
-            L[mt][0] = L[mt][1] = f32x4{b.x, b.y, b.z, b.w};
+#pragma unroll
+            for (int pt = 0; pt < PT; ++pt) L[mt][pt] = f32x4{b.x, b.y, b.z, b.w};
         }
 #pragma unroll
         for (int kc = 0; kc < CK; ++kc)
@@ -94,12 +98,12 @@ __global__ __launch_bounds__(256, 1) void k_deslice_wide(const bf16_t *__restric
             for (int mt = 0; mt < MT; ++mt) {
                 Frag<bf16_t> a;
                 a.v = *reinterpret_cast<const bf16x8 *>(wa + ((mt * CK + kc) * 64 + lane) * 16);
-                mma(L[mt][0], a, xb[0][kc]);
-                mma(L[mt][1], a, xb[1][kc]);
-            }
-        Frag<bf16_t> wb[2][KM];
 #pragma unroll
-        for (int pt = 0; pt < 2; ++pt) {
+                for (int pt = 0; pt < PT; ++pt) mma(L[mt][pt], a, xb[pt][kc]);
+            }
+        Frag<bf16_t> wb[PT][KM];
+#pragma unroll
+        for (int pt = 0; pt < PT; ++pt) {
             float mx = L[0][pt][0];
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt)
@@ -130,14 +134,14 @@ __global__ __launch_bounds__(256, 1) void k_deslice_wide(const bf16_t *__restric
             for (int km = 0; km < KM; ++km) {
                 Frag<bf16_t> a;
                 a.v = *reinterpret_cast<const bf16x8 *>(za + ((ct * KM + km) * 64 + lane) * 16);
-                mma(O[ct][0], a, wb[0][km]);
-                mma(O[ct][1], a, wb[1][km]);
+#pragma unroll
+                for (int pt = 0; pt < PT; ++pt) mma(O[ct][pt], a, wb[pt][km]);
             }
     }
 
     // Tiles ct = 2k, 2k+1 hold channels 32k + 8g + 4(ct & 1) + r of point p.
 #pragma unroll
-    for (int pt = 0; pt < 2; ++pt) {
+    for (int pt = 0; pt < PT; ++pt) {
         const int64_t p = p0 + 16 * pt + li;
         if (p >= n) continue;
 #pragma unroll
