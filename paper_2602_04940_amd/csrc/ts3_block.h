@@ -18,8 +18,9 @@
 //
 // k_mlp_residual: 128 points per workgroup, as eight waves of one 16-point
 // tile (the stack's choice: two waves per SIMD hide each other's GELU and
-// LDS latency) or four waves of two tiles.  Each wave keeps LN2(y) of its points as B fragments (K = channels)
-// in registers and the 16 x C output accumulator out^T[c][p]; the hidden layer
+// LDS latency) or four waves of two tiles.  Each wave keeps LN2(y) of its
+// points as B fragments (K = channels) in registers and the 16 x C output
+// accumulator out^T[c][p]; the hidden layer
 // is walked in 64-unit chunks staged in LDS (two slots, one chunk ahead):
 //   GEMM1  H^T[f][p] = W_a^T[f][:] . LN2(y)[p][:] + b_a[f]   (A = staged W_a^T)
 //   GELU   in registers; the 16 x 4 outputs of two hidden tiles are exactly a
@@ -245,15 +246,30 @@ __global__ __launch_bounds__(512 / PT, 1) void k_mlp_residual(
 #pragma unroll
             for (int pt = 0; pt < PT; ++pt) Hh[ht][pt] = f32x4{b.x, b.y, b.z, b.w};
         }
+        // A fragments are read one K step (or channel tile) ahead of their
+        // products, so LDS latency overlaps the matrix cores.
+        Frag<bf16_t> a1[2][HT];
+        auto read1 = [&](int kc, Frag<bf16_t>(&dst)[HT]) {
 #pragma unroll
-        for (int kc = 0; kc < CK; ++kc)
+            for (int ht = 0; ht < HT; ++ht)
+                dst[ht].v = *reinterpret_cast<const bf16x8 *>(wa + ((ht * CK + kc) * 64 + lane) * 16);
+        };
+        read1(0, a1[0]);
 #pragma unroll
-            for (int ht = 0; ht < HT; ++ht) {
-                Frag<bf16_t> a;
-                a.v = *reinterpret_cast<const bf16x8 *>(wa + ((ht * CK + kc) * 64 + lane) * 16);
+        for (int kc = 0; kc < CK; ++kc) {
+            if (kc + 1 < CK) read1(kc + 1, a1[(kc + 1) & 1]);
 #pragma unroll
-                for (int pt = 0; pt < PT; ++pt) mma(Hh[ht][pt], a, yb[pt][kc]);
-            }
+            for (int ht = 0; ht < HT; ++ht)
+#pragma unroll
+                for (int pt = 0; pt < PT; ++pt) mma(Hh[ht][pt], a1[kc & 1][ht], yb[pt][kc]);
+        }
+        Frag<bf16_t> a2[2][KM];
+        auto read2 = [&](int ct, Frag<bf16_t>(&dst)[KM]) {
+#pragma unroll
+            for (int km = 0; km < KM; ++km)
+                dst[km].v = *reinterpret_cast<const bf16x8 *>(wb + ((ct * KM + km) * 64 + lane) * 16);
+        };
+        read2(0, a2[0]);  // in flight during the GELU
         Frag<bf16_t> hb[PT][KM];
 #pragma unroll
         for (int pt = 0; pt < PT; ++pt)
@@ -265,14 +281,13 @@ __global__ __launch_bounds__(512 / PT, 1) void k_mlp_residual(
                     hb[pt][km].set2(t, gelu_exact(Hh[ht][pt][t & 3]), gelu_exact(Hh[ht][pt][(t & 3) + 1]));
                 }
 #pragma unroll
-        for (int ct = 0; ct < CT; ++ct)
+        for (int ct = 0; ct < CT; ++ct) {
+            if (ct + 1 < CT) read2(ct + 1, a2[(ct + 1) & 1]);
 #pragma unroll
-            for (int km = 0; km < KM; ++km) {
-                Frag<bf16_t> a;
-                a.v = *reinterpret_cast<const bf16x8 *>(wb + ((ct * KM + km) * 64 + lane) * 16);
+            for (int km = 0; km < KM; ++km)
 #pragma unroll
-                for (int pt = 0; pt < PT; ++pt) mma(Z[ct][pt], a, hb[pt][km]);
-            }
+                for (int pt = 0; pt < PT; ++pt) mma(Z[ct][pt], a2[ct & 1][km], hb[pt][km]);
+        }
     }
 
     // out = x + pa + z + bb; lane (li, g) of tile pt holds channels

@@ -92,15 +92,30 @@ __global__ __launch_bounds__(512 / PT, 1) void k_deslice_wide(const bf16_t *__re
 #pragma unroll
             for (int pt = 0; pt < PT; ++pt) L[mt][pt] = f32x4{b.x, b.y, b.z, b.w};
         }
+        // A fragments are read one K step (or channel tile) ahead of their
+        // products, so LDS latency overlaps the matrix cores.
+        Frag<bf16_t> a1[2][MT];
+        auto read1 = [&](int kc, Frag<bf16_t>(&dst)[MT]) {
 #pragma unroll
-        for (int kc = 0; kc < CK; ++kc)
+            for (int mt = 0; mt < MT; ++mt)
+                dst[mt].v = *reinterpret_cast<const bf16x8 *>(wa + ((mt * CK + kc) * 64 + lane) * 16);
+        };
+        read1(0, a1[0]);
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
-                Frag<bf16_t> a;
-                a.v = *reinterpret_cast<const bf16x8 *>(wa + ((mt * CK + kc) * 64 + lane) * 16);
+        for (int kc = 0; kc < CK; ++kc) {
+            if (kc + 1 < CK) read1(kc + 1, a1[(kc + 1) & 1]);
 #pragma unroll
-                for (int pt = 0; pt < PT; ++pt) mma(L[mt][pt], a, xb[pt][kc]);
-            }
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int pt = 0; pt < PT; ++pt) mma(L[mt][pt], a1[kc & 1][mt], xb[pt][kc]);
+        }
+        Frag<bf16_t> a2[2][KM];
+        auto read2 = [&](int ct, Frag<bf16_t>(&dst)[KM]) {
+#pragma unroll
+            for (int km = 0; km < KM; ++km)
+                dst[km].v = *reinterpret_cast<const bf16x8 *>(za + ((ct * KM + km) * 64 + lane) * 16);
+        };
+        read2(0, a2[0]);  // in flight during the softmax
         Frag<bf16_t> wb[PT][KM];
 #pragma unroll
         for (int pt = 0; pt < PT; ++pt) {
@@ -129,14 +144,13 @@ __global__ __launch_bounds__(512 / PT, 1) void k_deslice_wide(const bf16_t *__re
                 }
         }
 #pragma unroll
-        for (int ct = 0; ct < CT; ++ct)
+        for (int ct = 0; ct < CT; ++ct) {
+            if (ct + 1 < CT) read2(ct + 1, a2[(ct + 1) & 1]);
 #pragma unroll
-            for (int km = 0; km < KM; ++km) {
-                Frag<bf16_t> a;
-                a.v = *reinterpret_cast<const bf16x8 *>(za + ((ct * KM + km) * 64 + lane) * 16);
+            for (int km = 0; km < KM; ++km)
 #pragma unroll
-                for (int pt = 0; pt < PT; ++pt) mma(O[ct][pt], a, wb[pt][km]);
-            }
+                for (int pt = 0; pt < PT; ++pt) mma(O[ct][pt], a2[ct & 1][km], wb[pt][km]);
+        }
     }
 
     // Tiles ct = 2k, 2k+1 hold channels 32k + 8g + 4(ct & 1) + r of point p.
