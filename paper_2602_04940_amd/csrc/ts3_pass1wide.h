@@ -138,13 +138,15 @@ __global__ __launch_bounds__(256, 1) void k_slice_accumulate_wide(
                 const int R = prow(pt, li);
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) L[mt][pt] = bias[mt];
+                // all K steps' x operands first, so their LDS latency overlaps
+                Frag<bf16_t> xb[CK];
 #pragma unroll
-                for (int kc = 0; kc < CK; ++kc) {
-                    Frag<bf16_t> xb;
-                    xb.v = *reinterpret_cast<const bf16x8 *>(tile + xoff<XROW>(R, (kc * 32 + g * 8) * 2));
+                for (int kc = 0; kc < CK; ++kc)
+                    xb[kc].v = *reinterpret_cast<const bf16x8 *>(tile + xoff<XROW>(R, (kc * 32 + g * 8) * 2));
 #pragma unroll
-                    for (int mt = 0; mt < MT; ++mt) mma(L[mt][pt], w2[mt][kc], xb);
-                }
+                for (int kc = 0; kc < CK; ++kc)
+#pragma unroll
+                    for (int mt = 0; mt < MT; ++mt) mma(L[mt][pt], w2[mt][kc], xb[kc]);
             }
             unsigned char *wt = wtiles + wave * WTILE;
 #pragma unroll
@@ -187,13 +189,13 @@ __global__ __launch_bounds__(256, 1) void k_slice_accumulate_wide(
             if (wave == 0)
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) mma(D[mt], a[mt], ones);
+            Frag<bf16_t> bx[CTW];  // read before the products, as above
 #pragma unroll
-            for (int ct = 0; ct < CTW; ++ct) {
-                Frag<bf16_t> bx;
-                tr_frag<XROW>(bx, tr_addr<XROW, true>(xt, g, wave * CW + ct * 16, li));
+            for (int ct = 0; ct < CTW; ++ct) tr_frag<XROW>(bx[ct], tr_addr<XROW, true>(xt, g, wave * CW + ct * 16, li));
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt) mma(S[mt][ct], a[mt], bx);
-            }
+            for (int ct = 0; ct < CTW; ++ct)
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) mma(S[mt][ct], a[mt], bx[ct]);
         }
     }
 
