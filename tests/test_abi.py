@@ -76,6 +76,35 @@ def test_null_arguments():
     assert lib.ts3_status_string(L.TS3_ERR_BAD_STATE) == b"call out of order"
 
 
+def test_block_weight_layout_matches_header():
+    assert ct.sizeof(L.BlockWeights) == 17 * ct.sizeof(ct.c_void_p)
+    assert L.BlockWeights.ln1_g.offset == ct.sizeof(L.Weights)
+
+
+@pytest.mark.parametrize("kw,blocks,hidden,status", [
+    (dict(), 0, 512, L.TS3_ERR_INVALID_ARG),                                 # no blocks
+    (dict(), 2, 384, L.TS3_ERR_UNSUPPORTED),                                 # hidden != 4C
+    (dict(io_dtype=L.TS3_FP32), 2, 512, L.TS3_ERR_UNSUPPORTED),              # activations are bf16
+    (dict(C=256, H=8, dh=32, M=32), 2, 1024, L.TS3_ERR_UNSUPPORTED),         # no C=256, M=32 layer kernel
+    (dict(temperature=-1.0), 2, 512, L.TS3_ERR_INVALID_ARG),
+])
+def test_bad_stack_is_rejected_before_any_device_call(kw, blocks, hidden, status):
+    h = ct.c_void_p(1)
+    d = _desc(**kw)
+    assert L.lib().ts3_stack_create(ct.byref(d), blocks, hidden, ct.byref(h)) == status
+    assert h.value is None
+
+
+def test_stack_calls_reject_null_arguments():
+    lib = L.lib()
+    assert lib.ts3_stack_create(None, 1, 512, None) == L.TS3_ERR_INVALID_ARG
+    assert lib.ts3_stack_free(None) == L.TS3_OK
+    assert lib.ts3_stack_forward(None, None, None, 1, 1, 1, None) == L.TS3_ERR_INVALID_ARG
+    assert lib.ts3_stack_decode(None, None, None, 1, 1, None) == L.TS3_ERR_INVALID_ARG
+    assert lib.ts3_stack_feedforward(None, None, 0, None, None, 1, None, None) == L.TS3_ERR_INVALID_ARG
+    assert lib.ts3_stack_layer(None, 0, None) == L.TS3_ERR_INVALID_ARG
+
+
 def test_package_import_loads_nothing_and_product_has_no_oracle_dependency():
     import importlib
     import sys
