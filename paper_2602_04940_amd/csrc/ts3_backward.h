@@ -84,71 +84,85 @@ __device__ __forceinline__ void softmax_tile(f32x4 (&E)[MT], bool valid) {
         for (int r = 0; r < 4; ++r) E[mt][r] *= inv;
 }
 
-// Logits of head h for 16 points whose x rows start at xrow (lane row li):
-// E[mt] = b2s + W2'^T x, exp2-scaled (W2' = W2 log2(e) / tau).
-template <int C, int M>
-__device__ __forceinline__ void logits_tile(f32x4 (&E)[M / 16], const float *w2p, const float *b2s, int h,
-                                            const float *xrow, int lane) {
+// Logits of head h for NT 16-point tiles whose x rows start at xrow[t]
+// (lane row li): E[t][mt] = b2s + W2'^T x, exp2-scaled (W2' = W2 log2(e) /
+// tau).  Each A fragment (read from L2) serves all NT tiles.
+template <int C, int M, int NT>
+__device__ __forceinline__ void logits_tiles(f32x4 (&E)[NT][M / 16], const float *w2p, const float *b2s, int h,
+                                             const float *const (&xrow)[NT], int lane) {
     constexpr int MT = M / 16, CK = C / 32;
     const int g = lane >> 4;
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
         const float4 b = *reinterpret_cast<const float4 *>(b2s + h * M + mt * 16 + g * 4);
-        E[mt] = f32x4{b.x, b.y, b.z, b.w};
+#pragma unroll
+        for (int t = 0; t < NT; ++t) E[t][mt] = f32x4{b.x, b.y, b.z, b.w};
     }
     // K steps not unrolled: each step's fragments are loaded where they are
     // used (unrolled, the compiler hoists them all and spills).
 #pragma unroll 1
     for (int kc = 0; kc < CK; ++kc) {
-        Frag<float> xb;
-        frag_row(xb, xrow + 32 * kc, g);
+        Frag<float> xb[NT];
+#pragma unroll
+        for (int t = 0; t < NT; ++t) frag_row(xb[t], xrow[t] + 32 * kc, g);
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
             Frag<float> a;
             load8(a, w2p + ((((size_t)h * MT + mt) * CK + kc) * 64 + lane) * 8);
-            mma(E[mt], a, xb);
+#pragma unroll
+            for (int t = 0; t < NT; ++t) mma(E[t][mt], a, xb[t]);
         }
     }
 }
 
 // dw[m][p] = dd[h][m] + Z[h][m] . g_p + ds_raw[h][m] . x_p, then
-// dz = inv_tau * w * (dw - sum_m w dw) in place of dw (W holds w).
-template <int C, int M>
-__device__ __forceinline__ void dz_tile(f32x4 (&Dz)[M / 16], const f32x4 (&W)[M / 16], const float *Z,
-                                        const float *dsr, const float *dd, int h, const float *xrow,
-                                        const float *grow, float inv_tau, int lane) {
+// dz = inv_tau * w * (dw - sum_m w dw) in place of dw (W holds w), for NT
+// tiles sharing every A fragment.
+template <int C, int M, int NT>
+__device__ __forceinline__ void dz_tiles(f32x4 (&Dz)[NT][M / 16], const f32x4 (&W)[NT][M / 16], const float *Z,
+                                         const float *dsr, const float *dd, int h, const float *const (&xrow)[NT],
+                                         const float *const (&grow)[NT], float inv_tau, int lane) {
     constexpr int MT = M / 16, CK = C / 32;
     const int g = lane >> 4, li = lane & 15;
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
         const float4 b = *reinterpret_cast<const float4 *>(dd + h * M + mt * 16 + g * 4);
-        Dz[mt] = f32x4{b.x, b.y, b.z, b.w};
+#pragma unroll
+        for (int t = 0; t < NT; ++t) Dz[t][mt] = f32x4{b.x, b.y, b.z, b.w};
     }
 #pragma unroll 1
     for (int kc = 0; kc < CK; ++kc) {
-        Frag<float> gb, xb;
-        frag_row(gb, grow + 32 * kc, g);
-        frag_row(xb, xrow + 32 * kc, g);
+        Frag<float> gb[NT], xb[NT];
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            frag_row(gb[t], grow[t] + 32 * kc, g);
+            frag_row(xb[t], xrow[t] + 32 * kc, g);
+        }
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
             const size_t row = ((size_t)h * M + mt * 16 + li) * C + 32 * kc;
             Frag<float> a;
             frag_row(a, Z + row, g);
-            mma(Dz[mt], a, gb);
+#pragma unroll
+            for (int t = 0; t < NT; ++t) mma(Dz[t][mt], a, gb[t]);
             frag_row(a, dsr + row, g);
-            mma(Dz[mt], a, xb);
+#pragma unroll
+            for (int t = 0; t < NT; ++t) mma(Dz[t][mt], a, xb[t]);
         }
     }
-    float t = 0.f;
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
+    for (int t = 0; t < NT; ++t) {
+        float s = 0.f;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) t += W[mt][r] * Dz[mt][r];
-    t = xrow_sum(t);
+        for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
+            for (int r = 0; r < 4; ++r) s += W[t][mt][r] * Dz[t][mt][r];
+        s = xrow_sum(s);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) Dz[mt][r] = inv_tau * W[mt][r] * (Dz[mt][r] - t);
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) Dz[t][mt][r] = inv_tau * W[t][mt][r] * (Dz[t][mt][r] - s);
+    }
 }
 
 template <int C, int M> struct BwHeadCfg {
@@ -203,24 +217,35 @@ __global__ __launch_bounds__(256, 1) void k_bw_head(const float *__restrict__ x,
         const int64_t p0 = p_begin + ((int64_t)b << 5);
         // w (MODE 0) or dz (MODE 1) of the block's two 16-point tiles, as the
         // transposed tile tt[m][p].
+        {
+            bool valid[2];
+            const float *xr[2], *gr[2];
 #pragma unroll
-        for (int pt = 0; pt < 2; ++pt) {
-            const int64_t p = p0 + 16 * pt + li;
-            const bool valid = p < p_end;
-            const int64_t pc = valid ? p : p_end - 1;  // padding rows repeat the last point
-            f32x4 E[MT];
-            logits_tile<C, M>(E, w2p, b2s, h, x + pc * C, lane);
-            softmax_tile<MT>(E, valid);
+            for (int pt = 0; pt < 2; ++pt) {
+                const int64_t p = p0 + 16 * pt + li;
+                valid[pt] = p < p_end;
+                const int64_t pc = valid[pt] ? p : p_end - 1;  // padding rows repeat the last point
+                xr[pt] = x + pc * C;
+                gr[pt] = gout + pc * C;
+            }
+            f32x4 E[2][MT];
+            logits_tiles<C, M, 2>(E, w2p, b2s, h, xr, lane);
+#pragma unroll
+            for (int pt = 0; pt < 2; ++pt) softmax_tile<MT>(E[pt], valid[pt]);
             if constexpr (MODE == 1) {
-                f32x4 Dz[MT];
-                dz_tile<C, M>(Dz, E, Z, dsr, dd, h, x + pc * C, gout + pc * C, inv_tau, lane);
+                f32x4 Dz[2][MT];
+                dz_tiles<C, M, 2>(Dz, E, Z, dsr, dd, h, xr, gr, inv_tau, lane);
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt) E[mt] = Dz[mt];
+                for (int pt = 0; pt < 2; ++pt)
+#pragma unroll
+                    for (int mt = 0; mt < MT; ++mt) E[pt][mt] = Dz[pt][mt];
             }
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
+            for (int pt = 0; pt < 2; ++pt)
 #pragma unroll
-                for (int r = 0; r < 4; ++r) tt[(mt * 16 + g * 4 + r) * 32 + 16 * pt + li] = E[mt][r];
+                for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) tt[(mt * 16 + g * 4 + r) * 32 + 16 * pt + li] = E[pt][mt][r];
         }
         // The block's point rows, transposed: rt[c][p] (padding rows repeat the
         // last point; their weights are zero).
@@ -297,10 +322,13 @@ __global__ __launch_bounds__(256, 1) void k_bw_dx(const float *__restrict__ x, c
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct) O[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int h = 0; h < H; ++h) {
-        f32x4 E[MT], Dz[MT];
-        logits_tile<C, M>(E, w2p, b2s, h, xrow, lane);
-        softmax_tile<MT>(E, valid);
-        dz_tile<C, M>(Dz, E, Z, dsr, dd, h, xrow, grow, inv_tau, lane);
+        f32x4 E1[1][MT], Dz1[1][MT];
+        const float *xr[1] = {xrow}, *gr[1] = {grow};
+        logits_tiles<C, M, 1>(E1, w2p, b2s, h, xr, lane);
+        softmax_tile<MT>(E1[0], valid);
+        dz_tiles<C, M, 1>(Dz1, E1, Z, dsr, dd, h, xr, gr, inv_tau, lane);
+        f32x4(&E)[MT] = E1[0];
+        f32x4(&Dz)[MT] = Dz1[0];
 #pragma unroll
         for (int km = 0; km < KM; ++km) {
             Frag<float> wf, zf;
