@@ -171,12 +171,15 @@ void launch_bw_head(int mode, const float *x, const float *g, int64_t n, int64_t
                            nspan, H, w2p, b2s, Z, dsr, dd, inv_tau, partials);
 }
 
+constexpr int BW_DX_TILES_PER_WAVE = 2;  // each L2 A fragment serves two 16-point tiles
+
 template <int C, int M>
 void launch_bw_dx(const float *x, const float *g, int64_t n, int32_t H, const float *w2p, const float *b2s,
                   const float *W2, const float *Z, const float *dsr, const float *dsT, const float *dd,
                   float inv_tau, float *dx, hipStream_t st) {
-    hipLaunchKernelGGL((k_bw_dx<C, M>), dim3((unsigned)((n + 63) / 64)), dim3(256), 0, st, x, g, n, H, w2p, b2s,
-                       W2, Z, dsr, dsT, dd, inv_tau, dx);
+    constexpr int NT = BW_DX_TILES_PER_WAVE;
+    hipLaunchKernelGGL((k_bw_dx<C, M, NT>), dim3((unsigned)((n + 64 * NT - 1) / (64 * NT))), dim3(256), 0, st, x, g,
+                       n, H, w2p, b2s, W2, Z, dsr, dsT, dd, inv_tau, dx);
 }
 
 template <typename T, int C, int M> Kernels make_kernels() {

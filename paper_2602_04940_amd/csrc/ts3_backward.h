@@ -12,7 +12,7 @@
 //   k_bw_head<MODE 1>  per (span, head): recompute w; dw = g.Z + x.ds_raw +
 //                      dd; dz = (1/tau) w (dw - sum_m w dw); partial
 //                      dW2^T[m][:] = sum_p dz[p][m] x_p and db2 = sum_p dz
-//   k_bw_dx            per 16-point wave block over all heads: recompute w
+//   k_bw_dx            per wave block of 16-point tiles, over all heads: recompute w
 //                      and dz; dx = sum_h dz W2_h^T + w ds_raw_h
 //
 // Span partials are folded in index order by the forward's fold kernels, so
@@ -295,11 +295,12 @@ __global__ __launch_bounds__(256, 1) void k_bw_head(const float *__restrict__ x,
         dst[e] = (lds[e] + lds[E + e]) + (lds[2 * E + e] + lds[3 * E + e]);
 }
 
-// dx for 16-point wave blocks (four per workgroup): over the heads, recompute
-// w and dz, then dx[p][c] += sum_m dz[p][m] W2[c][hM+m] + w[p][m] ds_raw[h][m][c].
-// dsT is ds_raw transposed per head: [H][C][M].  W2 is the layer's (unscaled)
-// Linear2 weight [C][H*M].
-template <int C, int M>
+// dx for wave blocks of NT 16-point tiles (four waves per workgroup): over the
+// heads, recompute w and dz, then dx[p][c] += sum_m dz[p][m] W2[c][hM+m] +
+// w[p][m] ds_raw[h][m][c]; every A fragment (read from L2) serves the NT
+// tiles.  dsT is ds_raw transposed per head: [H][C][M].  W2 is the layer's
+// (unscaled) Linear2 weight [C][H*M].  Grid: ceil(n / (64 NT)) workgroups.
+template <int C, int M, int NT>
 __global__ __launch_bounds__(256, 1) void k_bw_dx(const float *__restrict__ x, const float *__restrict__ gout,
                                                   int64_t n, int32_t H, const float *__restrict__ w2p,
                                                   const float *__restrict__ b2s, const float *__restrict__ W2,
@@ -310,45 +311,61 @@ __global__ __launch_bounds__(256, 1) void k_bw_dx(const float *__restrict__ x, c
     const int lane = threadIdx.x & 63;
     const int wave = (int)(threadIdx.x >> 6);
     const int li = lane & 15, g = lane >> 4;
-    const int64_t p0 = ((int64_t)blockIdx.x * 4 + wave) * 16;
+    const int64_t p0 = ((int64_t)blockIdx.x * 4 + wave) * (16 * NT);
     if (p0 >= n) return;  // wave-uniform; the kernel has no barriers
-    const int64_t p = p0 + li;
-    const bool valid = p < n;
-    const int64_t pc = valid ? p : n - 1;
-    const float *xrow = x + pc * C, *grow = gout + pc * C;
+    bool valid[NT];
+    const float *xr[NT], *gr[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        const int64_t p = p0 + 16 * t + li;
+        valid[t] = p < n;
+        const int64_t pc = valid[t] ? p : n - 1;
+        xr[t] = x + pc * C;
+        gr[t] = gout + pc * C;
+    }
     const int HM = H * M;
 
-    f32x4 O[CT];
+    f32x4 O[NT][CT];
 #pragma unroll
-    for (int ct = 0; ct < CT; ++ct) O[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) O[t][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int h = 0; h < H; ++h) {
-        f32x4 E1[1][MT], Dz1[1][MT];
-        const float *xr[1] = {xrow}, *gr[1] = {grow};
-        logits_tiles<C, M, 1>(E1, w2p, b2s, h, xr, lane);
-        softmax_tile<MT>(E1[0], valid);
-        dz_tiles<C, M, 1>(Dz1, E1, Z, dsr, dd, h, xr, gr, inv_tau, lane);
-        f32x4(&E)[MT] = E1[0];
-        f32x4(&Dz)[MT] = Dz1[0];
+        f32x4 E[NT][MT], Dz[NT][MT];
+        logits_tiles<C, M, NT>(E, w2p, b2s, h, xr, lane);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) softmax_tile<MT>(E[t], valid[t]);
+        dz_tiles<C, M, NT>(Dz, E, Z, dsr, dd, h, xr, gr, inv_tau, lane);
 #pragma unroll
         for (int km = 0; km < KM; ++km) {
-            Frag<float> wf, zf;
-            pack_b<MT>(E, km, wf);
-            pack_b<MT>(Dz, km, zf);
+            Frag<float> wf[NT], zf[NT];
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                pack_b<MT>(E[t], km, wf[t]);
+                pack_b<MT>(Dz[t], km, zf[t]);
+            }
 #pragma unroll
             for (int ct = 0; ct < CT; ++ct) {
                 const int c = ct * 16 + li;
                 Frag<float> a;
                 frag_slices<M>(a, W2 + (size_t)c * HM + h * M, km, g);
-                mma(O[ct], a, zf);
+#pragma unroll
+                for (int t = 0; t < NT; ++t) mma(O[t][ct], a, zf[t]);
                 frag_slices<M>(a, dsT + ((size_t)h * C + c) * M, km, g);
-                mma(O[ct], a, wf);
+#pragma unroll
+                for (int t = 0; t < NT; ++t) mma(O[t][ct], a, wf[t]);
             }
         }
     }
-    if (valid)
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        const int64_t p = p0 + 16 * t + li;
+        if (!valid[t]) continue;
 #pragma unroll
         for (int ct = 0; ct < CT; ++ct)
-            *reinterpret_cast<float4 *>(dx + p * C + ct * 16 + g * 4) = float4{O[ct][0], O[ct][1], O[ct][2], O[ct][3]};
+            *reinterpret_cast<float4 *>(dx + p * C + ct * 16 + g * 4) =
+                float4{O[t][ct][0], O[t][ct][1], O[t][ct][2], O[t][ct][3]};
+    }
 }
 
 // Token side of the backward, one workgroup per head (256 threads):
