@@ -110,3 +110,28 @@ def test_decoding_from_injected_states():
     err = rel_l2(got, ref)
     print(f"injected-state decode rel L2 {err:.3e}", flush=True)
     assert err <= BF16_TOL
+
+
+def test_feedforward_half_matches_the_oracle_and_writes_the_next_layernorm():
+    import torch
+    C, H, M, L, n = 256, 8, 64, 2, 1000
+    F = 4 * C
+    banner(f"feed-forward half C={C} F={F} n={n} (ragged 128-point workgroups)")
+    rng = np.random.default_rng(23)
+    x64 = round_bf16(rng.standard_normal((n, C)))
+    pa64 = round_bf16(0.5 * rng.standard_normal((n, C)))
+    blocks = _blocks(C, H, M, F, L, seed=60)
+    dev = _dev_blocks(blocks)
+    with _stack(C, H, M, L, 1024, n) as st:
+        x = to_device(x64, "bf16")
+        xn = torch.empty_like(x)
+        st.feedforward(dev, 0, x, to_device(pa64, "bf16"), xn_next=xn)
+        torch.cuda.synchronize()
+        got, got_xn = to_host(x), to_host(xn)
+    b = _f64(blocks)
+    y = x64 + pa64
+    ref = y + BK.mlp(BK.layer_norm(y, b[0]["ln2_g"], b[0]["ln2_b"]), b[0]["Wa"], b[0]["ba"], b[0]["Wb"], b[0]["bb"])
+    err = rel_l2(got, ref)
+    err_n = rel_l2(got_xn, BK.layer_norm(ref, b[1]["ln1_g"], b[1]["ln1_b"]))
+    print(f"feed-forward rel L2 {err:.3e}, next LN1 rel L2 {err_n:.3e}", flush=True)
+    assert err <= BF16_TOL and err_n <= BF16_TOL
