@@ -23,9 +23,9 @@ def _torch():
     return torch
 
 
-def _layer(C, H, M, Q, N):
+def _layer(C, H, M, Q, N, accum="fp32"):
     from paper_2602_04940_amd import PhysicsAttention
-    return PhysicsAttention(C, H, M, C // H, 0.5, "fp32", group_span=Q, max_points=N)
+    return PhysicsAttention(C, H, M, C // H, 0.5, "fp32", group_span=Q, max_points=N, accum=accum)
 
 
 def _weights(W):
@@ -33,11 +33,11 @@ def _weights(W):
     return LayerWeights(W)
 
 
-def _gpu_backward(x64, g64, W, C, H, M, Q, tile):
+def _gpu_backward(x64, g64, W, C, H, M, Q, tile, accum="fp32"):
     torch = _torch()
     N = len(x64)
     x, g, lw = to_device(x64, "fp32"), to_device(g64, "fp32"), _weights(W)
-    with _layer(C, H, M, Q, N) as layer:
+    with _layer(C, H, M, Q, N, accum) as layer:
         layer.forward(lw, x, tile=tile, chunk=tile)
         dx, grads = layer.backward(lw, x, g, tile=tile)
         torch.cuda.synchronize()
@@ -79,3 +79,21 @@ def test_backward_is_tiling_independent_and_deterministic():
     assert np.array_equal(dx_a, dx_b) and np.array_equal(dx_a, dx_c)
     for k in NAMES:
         assert np.array_equal(ga[k], gb[k]) and np.array_equal(ga[k], gc[k]), k
+
+
+def test_backward_with_the_float64_fold_matches_oracle_and_is_tiling_independent():
+    C, H, M, N, Q = 128, 8, 64, 3000, 128
+    banner("backward with the float64 fold of span partials")
+    rng = np.random.default_rng(13)
+    x64 = rng.standard_normal((N, C)).astype(np.float32).astype(np.float64)
+    g64 = rng.standard_normal((N, C)).astype(np.float32).astype(np.float64)
+    W = make_weights(C, H, M, C // H, seed=7, bias_seed=8)
+    dx_a, ga = _gpu_backward(x64, g64, W, C, H, M, Q, 1024, accum="fp64")
+    dx_b, gb = _gpu_backward(x64, g64, W, C, H, M, Q, 384, accum="fp64")
+    assert np.array_equal(dx_a, dx_b)
+    for k in NAMES:
+        assert np.array_equal(ga[k], gb[k]), k
+    ref = BW.layer_backward(x64, {k: np.asarray(v, np.float64) for k, v in W.items()}, g64, H, M, 2.0)
+    assert normwise(dx_a, ref["dx"]) <= TOL
+    for k in NAMES:
+        assert normwise(ga[k], ref[k]) <= TOL, k
