@@ -66,31 +66,177 @@ def measured_traffic(kernel: str, launch_points: int):
 CAL_BYTES = 1 << 30  # calibration copy: 1 GiB read, 1 GiB written
 
 
-def pmc_driver(points: int):
-    """Short workload for rocprofv3 --pmc: two layer forwards over `points`
-    points (1M-point launches), then one device-to-device copy of CAL_BYTES whose
-    counter readings calibrate FETCH_SIZE / WRITE_SIZE."""
+def pmc_driver(points: int, workloads=("layer",)):
+    """Short workload for rocprofv3 --pmc runs.  "layer": two layer forwards over
+    `points` points of the 100M-point volume mesh's recipe (1M-point launches);
+    "stack": one block's feed-forward and both passes at C=256 on 1M car-surface
+    points; "backward": a float32 forward and backward on 1M volume points.
+    Ends with one device-to-device copy of CAL_BYTES whose counter readings
+    calibrate FETCH_SIZE / WRITE_SIZE."""
     import torch
 
-    from paper_2602_04940_amd import LayerWeights, PhysicsAttention
-    from ts3_synth import WORKLOADS, make_weights
-    from ts3_synth.device_gen import DeviceVolume
-    wl = WORKLOADS["volume_100m_bf16"]
-    x = torch.empty((points, wl.C), device="cuda", dtype=torch.bfloat16)
-    DeviceVolume(wl.seed, wl.C).fill(x)
-    out = torch.empty_like(x)
-    lw = LayerWeights(make_weights(wl.C, wl.H, wl.M, wl.dh, seed=0))
-    with PhysicsAttention(wl.C, wl.H, wl.M, wl.dh, wl.tau, "bf16", group_span=wl.group_span,
-                          max_points=points) as layer:
-        for _ in range(2):
-            layer.forward(lw, x, tile=wl.tile, chunk=wl.chunk, out=out)
+    from paper_2602_04940_amd import BlockWeights, LayerWeights, PhysicsAttention, TransolverStack
+    from ts3_synth import WORKLOADS, make_block_weights, make_weights
+    from ts3_synth.device_gen import DeviceSurface, DeviceVolume
+    if "layer" in workloads:
+        wl = WORKLOADS["volume_100m_bf16"]
+        x = torch.empty((points, wl.C), device="cuda", dtype=torch.bfloat16)
+        DeviceVolume(wl.seed, wl.C).fill(x)
+        out = torch.empty_like(x)
+        lw = LayerWeights(make_weights(wl.C, wl.H, wl.M, wl.dh, seed=0))
+        with PhysicsAttention(wl.C, wl.H, wl.M, wl.dh, wl.tau, "bf16", group_span=wl.group_span,
+                              max_points=points) as layer:
+            for _ in range(2):
+                layer.forward(lw, x, tile=wl.tile, chunk=wl.chunk, out=out)
+            torch.cuda.synchronize()
+        del x, out
+        log("pmc driver: layer done")
+    if "stack" in workloads:
+        wl = WORKLOADS["car_10m_bf16"]
+        n, F = 1_000_000, 4 * wl.C
+        x = torch.empty((n, wl.C), device="cuda", dtype=torch.bfloat16)
+        DeviceSurface(wl.seed, wl.C).fill(x)
+        blocks = [BlockWeights(make_block_weights(wl.C, wl.H, wl.M, wl.dh, F, seed=100 + l)) for l in range(2)]
+        stack = TransolverStack(wl.C, wl.H, wl.M, 2, F, wl.dh, wl.tau, group_span=wl.group_span, max_points=n)
+        stack.forward(blocks, x, tile=wl.tile, chunk=wl.chunk)
         torch.cuda.synchronize()
+        stack.close()
+        del x
+        log("pmc driver: stack done")
+    if "backward" in workloads:
+        wl = WORKLOADS["volume_2m_fp32"]
+        n = 1_000_000
+        x = torch.empty((n, wl.C), device="cuda", dtype=torch.float32)
+        DeviceVolume(wl.seed, wl.C, dtype=torch.float32).fill(x)
+        gen = torch.Generator(device="cuda")
+        gen.manual_seed(wl.seed + 1000)
+        g = torch.randn((n, wl.C), device="cuda", dtype=torch.float32, generator=gen)
+        lw = LayerWeights(make_weights(wl.C, wl.H, wl.M, wl.dh, seed=0))
+        with PhysicsAttention(wl.C, wl.H, wl.M, wl.dh, wl.tau, "fp32", group_span=wl.group_span,
+                              max_points=n) as layer:
+            layer.forward(lw, x, tile=wl.tile, chunk=wl.chunk)
+            layer.backward(lw, x, g, tile=wl.tile)
+            torch.cuda.synchronize()
+        del x, g
+        log("pmc driver: backward done")
     src = torch.empty(CAL_BYTES, device="cuda", dtype=torch.uint8).fill_(1)
     dst = torch.empty_like(src)
     torch.cuda.synchronize()
     dst.copy_(src)
     torch.cuda.synchronize()
     log("pmc driver done")
+
+
+# Kernels whose counters are summarised: name prefix -> (points per dispatch,
+# matrix flop per point that the kernel executes, algorithmic HBM bytes per
+# point, peak TFLOP/s of its matrix dtype).  Forward passes execute 4*C*H*M
+# (logits and one contraction); the backward's head kernels 4 and 8 and its dx
+# kernel 10 (x C*H*M), of which the backward as a whole needs 14.
+SQ_COUNTERS = ("SQ_INSTS_MFMA SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU SQ_INSTS_VALU_TRANS_F32 "
+               "SQ_INSTS_LDS SQ_LDS_BANK_CONFLICT SQ_LDS_IDX_ACTIVE SQ_BUSY_CYCLES GRBM_GUI_ACTIVE")
+COUNTER_KERNELS = {
+    "k_slice_accumulate_pc<": (1_000_000, 4 * 128 * 512, 256, PEAK_BF16_TFLOPS),
+    "k_deslice_w8<": (1_000_000, 4 * 128 * 512, 512, PEAK_BF16_TFLOPS),
+    "k_slice_accumulate_wide<": (1_000_000, 4 * 256 * 512, 512, PEAK_BF16_TFLOPS),
+    "k_deslice_wide<": (1_000_000, 4 * 256 * 512, 1024, PEAK_BF16_TFLOPS),
+    "k_mlp_residual<": (1_000_000, 4 * 256 * 1024, 1536, PEAK_BF16_TFLOPS),
+    "k_bw_head<128, 64, 0>": (1_000_000, 4 * 128 * 512, 1024, 157.3),
+    "k_bw_head<128, 64, 1>": (1_000_000, 8 * 128 * 512, 1024, 157.3),
+    "k_bw_dx<": (1_000_000, 10 * 128 * 512, 1536, 157.3),
+}
+
+
+def summarize_counters(sq_dir: str, fetch_dir: str, write_dir: str, command: str, out_path: str):
+    """Per-kernel counter summary (text) from three rocprofv3 runs of --pmc-driver:
+    the SQ/GRBM counters with --kernel-trace, then FETCH_SIZE, then WRITE_SIZE."""
+    import csv
+    import glob
+
+    def rows(d, pattern):
+        f = glob.glob(os.path.join(d, "**", pattern), recursive=True)
+        if not f:
+            raise SystemExit(f"no {pattern} under {d}")
+        return list(csv.DictReader(open(f[0])))
+
+    def per_kernel(rs, name):
+        acc = {}
+        for r in rs:
+            if r["Counter_Name"] != name:
+                continue
+            for k in COUNTER_KERNELS:
+                if k in r["Kernel_Name"]:
+                    acc.setdefault(k, []).append(float(r["Counter_Value"]))
+        return {k: sum(v) / len(v) for k, v in acc.items()}, {k: len(v) for k, v in acc.items()}
+
+    sq = rows(sq_dir, "*counter_collection.csv")
+    # GRBM_GUI_ACTIVE comes summed over the XCDs; the SQ counters over every
+    # CU and SIMD.  Shapes from the agent table of the same run.
+    gpu = [a for a in rows(sq_dir, "*agent_info.csv") if int(a.get("Simd_Count", 0) or 0) > 0][0]
+    n_xcc, n_cu, n_simd = int(gpu["Num_Xcc"]), int(gpu["Cu_Count"]), int(gpu["Simd_Count"])
+    trace = rows(sq_dir, "*kernel_trace.csv")
+    dur = {}
+    for r in trace:
+        for k in COUNTER_KERNELS:
+            if k in r["Kernel_Name"]:
+                dur.setdefault(k, []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9)
+    vals = {}
+    ndisp = {}
+    for name in SQ_COUNTERS.split():
+        v, n = per_kernel(sq, name)
+        vals[name] = v
+        ndisp.update(n)
+    fac = {}
+    for name, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        rs = rows(d, "*counter_collection.csv")
+        cal = [r for r in rs if r["Counter_Name"] == name and "copyBuffer" in r["Kernel_Name"]][-1]
+        fac[name] = CAL_BYTES / (float(cal["Counter_Value"]) * 1024.0)
+        vals[name] = per_kernel(rs, name)[0]
+    lines = [f"rocprofv3 counters per dispatch (averages over the dispatches of each kernel), one MI355X",
+             f"command: {command}",
+             f"calibration: FETCH_SIZE x{fac['FETCH_SIZE']:.4f}, WRITE_SIZE x{fac['WRITE_SIZE']:.4f} bytes per "
+             f"counted byte (a {CAL_BYTES >> 20} MiB device-to-device copy)",
+             "duration: kernel-trace average of the SQ run (counter collection serialises dispatches)",
+             f"GPU: {n_xcc} XCDs, {n_cu} CUs, {n_simd} SIMDs; cycles = GRBM_GUI_ACTIVE / {n_xcc} (the counter is summed "
+             "over the XCDs); clock = cycles / duration;",
+             "mfma%: SQ_VALU_MFMA_BUSY_CYCLES / (cycles x SIMDs); lds%: SQ_LDS_IDX_ACTIVE / (cycles x CUs); "
+             "bank%: SQ_LDS_BANK_CONFLICT / (cycles x CUs);",
+             "frac: executed matrix flop / duration / the dtype's dense peak; HBM: FETCH_SIZE + WRITE_SIZE, calibrated",
+             ""]
+    hdr = (f"{'kernel':26s} {'disp':>4s} {'us':>8s} {'GHz':>5s} {'TF/s':>7s} {'frac':>6s} {'mfma%':>6s} "
+           f"{'VALU/MFMA':>9s} {'TRANS/MFMA':>10s} {'LDS/MFMA':>8s} {'lds%':>5s} {'bank%':>6s} {'HBM MB':>8s} "
+           f"{'algo MB':>8s} {'GB/s':>7s}")
+    lines.append(hdr)
+    out = {}
+    for k, (pts, flop_pt, bytes_pt, peak) in COUNTER_KERNELS.items():
+        if k not in dur or k not in vals["SQ_INSTS_MFMA"]:
+            continue
+        t = sum(dur[k]) / len(dur[k])
+        g = vals["GRBM_GUI_ACTIVE"].get(k, float("nan")) / n_xcc
+        mf = vals["SQ_INSTS_MFMA"][k]
+        busy = vals["SQ_VALU_MFMA_BUSY_CYCLES"].get(k, float("nan"))
+        hbm = (vals["FETCH_SIZE"].get(k, float("nan")) * fac["FETCH_SIZE"] +
+               vals["WRITE_SIZE"].get(k, float("nan")) * fac["WRITE_SIZE"]) * 1024
+        tf = flop_pt * pts / t / 1e12
+        row = {"dispatches": ndisp.get(k), "us": t * 1e6, "clock_ghz": g / t / 1e9, "tflops": tf,
+               "frac": tf / peak, "mfma_busy": busy / (g * n_simd) if g else None,
+               "valu_per_mfma": vals["SQ_INSTS_VALU"][k] / mf, "trans_per_mfma":
+               vals["SQ_INSTS_VALU_TRANS_F32"][k] / mf, "lds_per_mfma": vals["SQ_INSTS_LDS"][k] / mf,
+               "lds_busy": vals["SQ_LDS_IDX_ACTIVE"][k] / (g * n_cu) if g else None,
+               "bank_conflict": vals["SQ_LDS_BANK_CONFLICT"][k] / (g * n_cu) if g else None,
+               "hbm_mb": hbm / 1e6, "algo_mb": bytes_pt * pts / 1e6, "gbs": hbm / t / 1e9}
+        out[k] = row
+        lines.append(f"{k.rstrip('<'):26s} {row['dispatches']:4d} {row['us']:8.1f} {row['clock_ghz']:5.2f} "
+                     f"{tf:7.1f} {row['frac']:6.3f} {100 * row['mfma_busy']:6.1f} {row['valu_per_mfma']:9.2f} "
+                     f"{row['trans_per_mfma']:10.2f} {row['lds_per_mfma']:8.2f} {100 * row['lds_busy']:5.1f} "
+                     f"{100 * row['bank_conflict']:6.2f} "
+                     f"{row['hbm_mb']:8.1f} {row['algo_mb']:8.1f} {row['gbs']:7.0f}")
+    lines += ["", f"kernel source hash {kernel_source_hash()}"]
+    text = "\n".join(lines) + "\n"
+    os.makedirs(os.path.dirname(out_path) or ".", exist_ok=True)
+    with open(out_path, "w") as fh:
+        fh.write(text)
+    print(text)
+    return out
 
 
 def summarize_traffic(fetch_dir: str, write_dir: str, command: str):
@@ -128,23 +274,56 @@ def summarize_traffic(fetch_dir: str, write_dir: str, command: str):
     print(json.dumps(out, indent=1))
 
 
-def cpu_baseline(x_dev, W, wl, sample):
-    """The float64 oracle (as written) on the first `sample` points, host cores."""
+def cpu_baseline_and_parity(x_dev, W, lw, wl, sample):
+    """The float64 oracle (as written) on the first `sample` points of the mesh,
+    taken as a mesh of its own, on a pool of host processes (one core each):
+    pass 1 over 65,536-point tiles summed in tile order, the token side, pass 2
+    over 65,536-point chunks.  Then the GPU layer runs the same sample with the
+    benchmark's launch configuration, and its state and output are compared
+    with the oracle's: the parity of this run."""
     import numpy as np
-    from threadpoolctl import threadpool_info
 
-    import oracle
-    xs = x_dev[:sample].float().cpu().numpy().astype(np.float64)
+    from oracle.pool import OraclePool
+    from paper_2602_04940_amd import PhysicsAttention, _lib as L
+    xs = x_dev[:sample]
+    x64 = xs.float().cpu().numpy().astype(np.float64)
     it = 1.0 / wl.tau
-    t0 = time.perf_counter()
-    st = oracle.build_state(xs, W, wl.H, wl.M, it, tile=wl.tile)
-    for c in range(0, sample, wl.chunk):
-        oracle.deslice(xs[c:c + wl.chunk], W["W2"], W["b2"], st["Z"], W["b3"], wl.H, wl.M, it)
-    dt = time.perf_counter() - t0
-    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
-    return {"value": sample / dt, "unit": "points/s", "cores": threads, "kind": "oracle",
-            "sample": f"layer forward (pass 1, state, pass 2) in float64 numpy on the first {sample} "
-                      f"points of the mesh: {dt:.1f} s"}
+    with OraclePool() as pool:
+        pool.sums([x64[:64]], W["W2"], W["b2"], wl.H, wl.M, it)  # workers started before the clock
+        t0 = time.perf_counter()
+        st = pool.state(x64, W, wl.H, wl.M, it, tile=65536)
+        ref = pool.decode(x64, W["W2"], W["b2"], st["Z"], W["b3"], wl.H, wl.M, it, chunk=65536)
+        dt = time.perf_counter() - t0
+        workers = pool.workers
+    base = {"value": sample / dt, "unit": "points/s", "cores": workers, "kind": "oracle",
+            "sample": f"layer forward (pass 1, state, pass 2) in float64 numpy on the first {sample} points of "
+                      f"the mesh as their own mesh, {workers} processes of one core each: {dt:.1f} s"}
+    import torch
+    with PhysicsAttention(wl.C, wl.H, wl.M, wl.dh, wl.tau, "bf16", group_span=wl.group_span,
+                          max_points=sample) as layer:
+        out = layer.forward(lw, xs, tile=wl.tile, chunk=wl.chunk)
+        torch.cuda.synchronize()
+        g_sr, g_d, g_z = layer.get(L.TS3_S_RAW), layer.get(L.TS3_D), layer.get(L.TS3_ZP)
+    got = out.float().cpu().numpy().astype(np.float64)
+
+    def rel(a, b):
+        return float(np.linalg.norm(a - b) / np.linalg.norm(b))
+
+    nb = sample // 256
+    d2 = ((got[:nb * 256] - ref[:nb * 256]) ** 2).sum(axis=1).reshape(nb, 256).sum(axis=1)
+    r2 = (ref[:nb * 256] ** 2).sum(axis=1).reshape(nb, 256).sum(axis=1)
+    rn = np.linalg.norm(ref, axis=1)
+    row = np.linalg.norm(got - ref, axis=1) / np.maximum(rn, np.sqrt((rn ** 2).mean()))
+    HM = wl.H * wl.M
+    tok = np.linalg.norm((g_sr - st["s_raw"]).reshape(HM, -1), axis=1) / np.linalg.norm(
+        st["s_raw"].reshape(HM, -1), axis=1)
+    parity = {"sample": f"first {sample} points as their own mesh, group span {wl.group_span}, "
+                        f"{wl.tile}-point tiles and chunks",
+              "bar": 0.02, "out_rel_l2": rel(got, ref), "out_worst_256_block": float(np.sqrt(d2 / r2).max()),
+              "out_worst_row": float(row.max()), "s_raw_worst_token": float(tok.max()),
+              "d_worst_rel": float((np.abs(g_d - st["d"]) / st["d"]).max()), "Z_rel_l2": rel(g_z, st["Z"])}
+    parity["pass"] = all(v <= 0.02 for k, v in parity.items() if k not in ("sample", "bar"))
+    return base, parity
 
 
 METRIC_BW = "mesh points/s per Physics-Attention layer fwd+bwd @2M pts C=128 fp32; % roofline"
@@ -164,7 +343,7 @@ def cpu_baseline_backward(x_dev, g_dev, W, wl, sample):
     t0 = time.perf_counter()
     BW.layer_backward(xs, W64, gs, wl.H, wl.M, 1.0 / wl.tau, tile=wl.tile)
     dt = time.perf_counter() - t0
-    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    threads = min(max([p.get("num_threads", 1) for p in threadpool_info()] + [1]), len(os.sched_getaffinity(0)))
     return {"value": sample / dt, "unit": "points/s", "cores": threads, "kind": "oracle",
             "sample": f"layer forward state + backward (all gradients) in float64 numpy on the first {sample} "
                       f"points of the mesh: {dt:.1f} s"}
@@ -270,7 +449,7 @@ def cpu_baseline_stack(x_dev, blocks, wl, sample):
     t0 = time.perf_counter()
     BK.stack_forward(xs, b64, wl.H, wl.M, 1.0 / wl.tau)
     dt = time.perf_counter() - t0
-    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    threads = min(max([p.get("num_threads", 1) for p in threadpool_info()] + [1]), len(os.sched_getaffinity(0)))
     return {"value": sample / dt, "unit": "points/s", "cores": threads, "kind": "oracle",
             "sample": f"{len(blocks)}-block stack forward in float64 numpy on the first {sample} points of the "
                       f"mesh (as their own mesh): {dt:.1f} s"}
@@ -390,9 +569,13 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--points", type=int, default=None, help="override N (quick runs)")
-    ap.add_argument("--cpu-sample", type=int, default=1_000_000)
+    ap.add_argument("--cpu-sample", type=int, default=2_000_000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--pmc-driver", action="store_true", help="short workload for rocprofv3 --pmc runs")
+    ap.add_argument("--pmc-workloads", default="layer",
+                    help="comma list of layer,stack,backward for --pmc-driver")
+    ap.add_argument("--summarize-counters", nargs=4, metavar=("SQ_DIR", "FETCH_DIR", "WRITE_DIR", "OUT"),
+                    help="per-kernel counter summary from three rocprofv3 runs of --pmc-driver")
     ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="write profiles/traffic.json from two --pmc runs of --pmc-driver")
     ap.add_argument("--command", default="", help="command line recorded with --summarize-traffic")
@@ -408,8 +591,11 @@ def main():
     if args.summarize_traffic:
         summarize_traffic(*args.summarize_traffic, args.command)
         return
+    if args.summarize_counters:
+        summarize_counters(*args.summarize_counters[:3], args.command, args.summarize_counters[3])
+        return
     if args.pmc_driver:
-        pmc_driver(args.points or 4_000_000)
+        pmc_driver(args.points or 4_000_000, tuple(args.pmc_workloads.split(",")))
         return
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU; --gpus {args.gpus} is not supported "
@@ -447,8 +633,11 @@ def main():
     lw = LayerWeights(W, dev)
     layer = PhysicsAttention(wl.C, wl.H, wl.M, wl.dh, wl.tau, "bf16", group_span=wl.group_span, max_points=N,
                              accum=args.accum)
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()  # drop the generator's cached blocks: what remains is x, out and the state
     free, total = torch.cuda.mem_get_info()
     hbm_used_gb = (total - free) / 1e9
+    layer_bytes = 2 * x.numel() * x.element_size() + layer.bytes()
 
     for i in range(args.warmup):
         layer.forward(lw, x, tile=wl.tile, chunk=wl.chunk, out=out)
@@ -492,9 +681,11 @@ def main():
     pts_launch = min(wl.tile, N)
     achieved = flop_per_point * pts_launch / (t_launch * 1e-3) / 1e12
     traffic = measured_traffic(kname, pts_launch)
+    layer_tflops = 2 * flop_per_point * N / (ms * 1e-3) / 1e12   # both passes over the timed step
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic, "kernel": kname,
-                "launch_ms": round(t_launch, 4), "launches": nl}
+                "launch_ms": round(t_launch, 4), "launches": nl,
+                "layer_achieved": round(layer_tflops, 2), "layer_frac": round(layer_tflops / PEAK_BF16_TFLOPS, 4)}
 
     result = {
         "metric": METRIC, "value": N / (ms * 1e-3), "unit": "points/s", "n_gpus": 1,
@@ -503,15 +694,18 @@ def main():
         "data": "synthetic: seeded volume mesh (box minus car-like body), Fourier features, device-generated",
         "config": {"workload": wl.name, "N": N, "C": wl.C, "H": wl.H, "M": wl.M, "dh": wl.dh, "tau": wl.tau,
                    "tile": wl.tile, "chunk": wl.chunk, "group_span": wl.group_span, "accum": args.accum,
-                   "hbm_used_gb": round(hbm_used_gb, 2), "state_bytes": layer.bytes()},
+                   "hbm_used_gb": round(hbm_used_gb, 2), "hbm_layer_gb": round(layer_bytes / 1e9, 2),
+                   "state_bytes": layer.bytes()},
         "passes_ms": {"pass1": round(t_p1, 3), "state": round(t_mid, 3), "pass2": round(t_p2, 3)},
         "roofline": roofline,
         "cpu_baseline": None,
+        "parity": None,
     }
-    if not args.no_cpu_baseline:
-        log(f"timing the float64 oracle on {args.cpu_sample} points (host cores)")
-        result["cpu_baseline"] = cpu_baseline(x, W, wl, min(args.cpu_sample, N))
     layer.close()
+    if not args.no_cpu_baseline:
+        log(f"timing the float64 oracle on {args.cpu_sample} points (host processes), then parity on them")
+        result["cpu_baseline"], result["parity"] = cpu_baseline_and_parity(x, W, lw, wl, min(args.cpu_sample, N))
+        log(f"parity: {result['parity']}")
     print(json.dumps(result), flush=True)
 
 

@@ -193,6 +193,17 @@ ts3_status ts3_layer_backward(ts3_state *st, const ts3_weights *w, const void *x
 ts3_status ts3_state_get(const ts3_state *st, int32_t which, float *host_dst, int64_t n,
                          void *stream);
 
+/* Copy the span partials of spans [span0, span0 + nspan) to host memory, after
+ * synchronising `stream`: [nspan][H][M][C+1] floats, where columns 0..C-1 hold
+ * the sum over the span's points of w_i x_i and column C the sum of w_i.  These
+ * are the per-span terms of Eq. (4) before the ordered fold (finalize sums them
+ * in span order).  Every requested span must have been accumulated since the
+ * last reset, and no backward may have run since (it reuses the buffer):
+ * otherwise TS3_ERR_BAD_STATE.  n must equal nspan*H*M*(C+1).  For tests and
+ * inspection. */
+ts3_status ts3_state_get_spans(const ts3_state *st, int64_t span0, int64_t nspan, float *host_dst, int64_t n,
+                               void *stream);
+
 /* Test hook: overwrite the cached state Z (which == TS3_ZP) and b3 from host
  * memory (b3 may be NULL = zero), convert it to the decoding operand format,
  * and mark the state ATTENDED, so pass 2 can be checked on its own.  The W2/b2

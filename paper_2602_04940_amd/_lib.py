@@ -58,6 +58,7 @@ SIGNATURES = {
     "ts3_layer_backward": (ct.c_int, [_P, ct.POINTER(Weights), _P, _P, ct.c_int64, ct.c_int64, _P,
                                       ct.POINTER(Grads), _P]),
     "ts3_state_get": (ct.c_int, [_P, ct.c_int32, _P, ct.c_int64, _P]),
+    "ts3_state_get_spans": (ct.c_int, [_P, ct.c_int64, ct.c_int64, _P, ct.c_int64, _P]),
     "ts3_state_set": (ct.c_int, [_P, ct.POINTER(Weights), ct.c_int32, _P, ct.c_int64, _P, _P]),
     "ts3_stack_create": (ct.c_int, [ct.POINTER(Desc), ct.c_int32, ct.c_int32, ct.POINTER(_P)]),
     "ts3_stack_free": (ct.c_int, [_P]),

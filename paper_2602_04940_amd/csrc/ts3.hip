@@ -13,7 +13,6 @@
 
 #include "../../include/ts3.h"
 #include "ts3_pass1.h"
-#include "ts3_pass1w8.h"
 #include "ts3_pass1pc.h"
 #include "ts3_pass1wide.h"
 #include "ts3_backward.h"
@@ -81,13 +80,14 @@ void launch_pass1(const void *x, int64_t n, int64_t span0, int32_t Q, int32_t ns
                            (const bf16_t *)x, n, span0, Q, nspan, H, (const bf16_t *)w2p, b2s, partials);
     } else if constexpr (sizeof(T) == 2 && M >= 32 && C == 128) {
         // Two heads per workgroup whenever H is even (independently of the
-        // span count, so that every tiling sums a span the same way).
+        // span count, so that every tiling sums a span the same way); the one
+        // odd case, H = 1, takes the generic kernel.
         if (H % 2 == 0)
             hipLaunchKernelGGL((k_slice_accumulate_pc<C, M>), dim3(nspan * (H / 2)), dim3(512), 0, st,
                                (const bf16_t *)x, n, span0, Q, nspan, H, (const bf16_t *)w2p, b2s, partials);
         else
-            hipLaunchKernelGGL((k_slice_accumulate_w8<C, M>), dim3(nspan * H), dim3(512), 0, st,
-                               (const bf16_t *)x, n, span0, Q, nspan, H, (const bf16_t *)w2p, b2s, partials);
+            hipLaunchKernelGGL((k_slice_accumulate<T, C, M>), dim3(nspan * H), dim3(256), 0, st,
+                               (const T *)x, n, span0, Q, nspan, H, (const T *)w2p, b2s, partials);
     } else {
         hipLaunchKernelGGL((k_slice_accumulate<T, C, M>), dim3(nspan * H), dim3(256), 0, st,
                            (const T *)x, n, span0, Q, nspan, H, (const T *)w2p, b2s, partials);
@@ -151,12 +151,14 @@ hipError_t launch_pass2(const void *x, int64_t n, int32_t H, const void *w2p, co
             }
             return hipSuccess;
         }
-    }
-    {
+        // Every supported 16-bit shape fits the staged kernel's LDS (H*dh = C
+        // bounds H*M*C); a shape that does not has no decoding kernel.
+        return hipErrorInvalidConfiguration;
+    } else {
         hipLaunchKernelGGL((k_deslice<T, C, M>), dim3((unsigned)nblk), dim3(256), 0, st, (const T *)x, n, H,
                            (const T *)w2p, b2s, (const T *)zp, (T *)out);
+        return hipSuccess;
     }
-    return hipSuccess;
 }
 
 template <int C, int M>
@@ -228,6 +230,7 @@ struct ts3_state {
     int64_t span_hi = 0;
     int phase = PH_RESET;
     bool w2_ready = false;
+    bool partials_fwd = false;  // the partial buffer holds pass-1 span sums (not a backward's)
     const float *W2 = nullptr, *b2 = nullptr;
     // Second stream for ts3_layer_forward (default priority): consecutive
     // tiles and chunks alternate between it and the caller's stream, so one
@@ -426,6 +429,7 @@ ts3_status ts3_state_reset(ts3_state *st, void *stream) {
     st->span_hi = 0;
     st->phase = PH_RESET;
     st->w2_ready = false;
+    st->partials_fwd = false;
     st->W2 = st->b2 = nullptr;
     return TS3_OK;
 }
@@ -474,6 +478,7 @@ ts3_status ts3_slice_accumulate(ts3_state *st, const ts3_weights *w, const void 
     if (ragged) st->span_written[(size_t)(span0 + nspan - 1)] = 2;
     st->span_hi = std::max(st->span_hi, span0 + nspan);
     st->phase = PH_ACCUM;
+    st->partials_fwd = true;
     return TS3_OK;
 }
 
@@ -677,6 +682,7 @@ ts3_status ts3_layer_backward(ts3_state *st, const ts3_weights *w, const void *x
         return TS3_OK;
     };
     // dZ = sum_i w_i^T g_i (its column C, sum_i w_i, is not needed)
+    st->partials_fwd = false;  // the head passes reuse the span partial buffer
     ts3_status s = head_pass(0);
     if (s == TS3_OK) s = fold_partials(st, nspan_all, st->bdZ, st->bdd, hs);
     if (s != TS3_OK) return s;
@@ -726,6 +732,25 @@ ts3_status ts3_state_get(const ts3_state *st, int32_t which, float *host_dst, in
     if (st->phase < need) return fail(TS3_ERR_BAD_STATE, "buffer %d is not computed yet", which);
     hipStream_t hs = (hipStream_t)stream;
     HIP_TRY(hipMemcpyAsync(host_dst, src, (size_t)size * 4, hipMemcpyDeviceToHost, hs));
+    HIP_TRY(hipStreamSynchronize(hs));
+    return TS3_OK;
+}
+
+ts3_status ts3_state_get_spans(const ts3_state *st, int64_t span0, int64_t nspan, float *host_dst, int64_t n,
+                               void *stream) {
+    if (!st || !host_dst) return fail(TS3_ERR_INVALID_ARG, "NULL argument");
+    if (span0 < 0 || nspan <= 0 || span0 + nspan > st->nspan_max)
+        return fail(TS3_ERR_INVALID_ARG, "spans [%lld, %lld) outside the state's %lld spans", (long long)span0,
+                    (long long)(span0 + nspan), (long long)st->nspan_max);
+    if (n != nspan * st->E)
+        return fail(TS3_ERR_INVALID_ARG, "%lld spans hold %lld floats, not %lld", (long long)nspan,
+                    (long long)(nspan * st->E), (long long)n);
+    if (!st->partials_fwd) return fail(TS3_ERR_BAD_STATE, "no pass-1 span partials (reset, or a backward ran)");
+    for (int64_t i = span0; i < span0 + nspan; ++i)
+        if (!st->span_written[(size_t)i])
+            return fail(TS3_ERR_BAD_STATE, "span %lld has not been accumulated", (long long)i);
+    hipStream_t hs = (hipStream_t)stream;
+    HIP_TRY(hipMemcpyAsync(host_dst, st->partials + span0 * st->E, (size_t)n * 4, hipMemcpyDeviceToHost, hs));
     HIP_TRY(hipStreamSynchronize(hs));
     return TS3_OK;
 }

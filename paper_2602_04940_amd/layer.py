@@ -151,6 +151,13 @@ class PhysicsAttention:
                 "ts3_state_get")
         return a
 
+    def get_spans(self, span0: int, nspan: int) -> np.ndarray:
+        """Span partials [nspan, H, M, C+1] (columns :C sum w x, column C sum w)."""
+        a = np.empty((nspan, self.H, self.M, self.C + 1), dtype=np.float32)
+        L.check(L.lib().ts3_state_get_spans(self.h, span0, nspan, a.ctypes.data_as(ct.c_void_p), a.size,
+                                            _stream()), "ts3_state_get_spans")
+        return a
+
     def set_state(self, w: LayerWeights, Z: np.ndarray, b3: np.ndarray | None = None):
         Z = np.ascontiguousarray(Z, dtype=np.float32)
         b3p = None

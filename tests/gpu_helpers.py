@@ -28,3 +28,58 @@ def to_host(t):
 
 def banner(msg):
     print(f"\n[gpu case] {msg}", flush=True)
+
+
+def block_rel_l2(got, ref, block=256):
+    """Largest relative L2 over consecutive blocks of `block` rows (the last
+    block may be short): a single wrong block of a large array fails it."""
+    got = np.asarray(got, dtype=np.float64).reshape(len(got), -1)
+    ref = np.asarray(ref, dtype=np.float64).reshape(len(ref), -1)
+    n = len(ref)
+    if n == 0:
+        return 0.0
+    nb = -(-n // block)
+    pad = nb * block - n
+    d2 = np.pad(((got - ref) ** 2).sum(axis=1), (0, pad)).reshape(nb, block).sum(axis=1)
+    r2 = np.pad((ref ** 2).sum(axis=1), (0, pad)).reshape(nb, block).sum(axis=1)
+    return float(np.sqrt(d2 / np.maximum(r2, 1e-300)).max())
+
+
+def row_rel(got, ref):
+    """Largest per-row error ||got_i - ref_i|| / max(||ref_i||, rms row norm):
+    relative to the row itself, with rows much smaller than the array's typical
+    row measured against that typical size instead."""
+    got = np.asarray(got, dtype=np.float64).reshape(len(got), -1)
+    ref = np.asarray(ref, dtype=np.float64).reshape(len(ref), -1)
+    if len(ref) == 0:
+        return 0.0
+    rn = np.linalg.norm(ref, axis=1)
+    floor = np.sqrt((rn ** 2).mean())
+    return float((np.linalg.norm(got - ref, axis=1) / np.maximum(np.maximum(rn, floor), 1e-300)).max())
+
+
+def assert_bf16_close(got, ref, what, tol=2e-2, block=256):
+    """The bf16 bar applied globally and locally: relative L2 over the whole
+    array, over every block of `block` consecutive rows, and per row (see
+    row_rel).  Rows are points for outputs and slice tokens for states."""
+    g, b, r = rel_l2(got, ref), block_rel_l2(got, ref, block), row_rel(got, ref)
+    print(f"{what}: rel L2 {g:.3e}, worst {block}-row block {b:.3e}, worst row {r:.3e}", flush=True)
+    assert g <= tol, (what, "global", g)
+    assert b <= tol, (what, "block", b)
+    assert r <= tol, (what, "row", r)
+    return g, b, r
+
+
+def assert_state_close(st, ref, what, tol=2e-2):
+    """bf16-path state against the oracle: s_raw and Z per slice token (rows of
+    [H*M, C]), d element by element, each within the bf16 bar."""
+    H, M = np.asarray(ref["d"]).shape
+    for k in ("s_raw", "Z"):
+        if k in st:
+            assert_bf16_close(np.asarray(st[k]).reshape(H * M, -1), np.asarray(ref[k]).reshape(H * M, -1),
+                              f"{what} {k}", tol, block=M)
+    dr = np.asarray(ref["d"], dtype=np.float64)
+    dg = np.asarray(st["d"], dtype=np.float64)
+    ed = float((np.abs(dg - dr) / np.maximum(np.abs(dr), 1e-300)).max()) if dr.size else 0.0
+    print(f"{what} d: worst element rel {ed:.3e}", flush=True)
+    assert ed <= tol, (what, "d", ed)

@@ -7,7 +7,7 @@ and from injected states."""
 import numpy as np
 import pytest
 
-from gpu_helpers import banner, rel_l2, to_device, to_host
+from gpu_helpers import assert_bf16_close, banner, rel_l2, to_device, to_host
 from oracle import block as BK
 from ts3_synth import make_block_weights, round_bf16
 
@@ -55,9 +55,7 @@ def test_stack_matches_oracle_and_is_tiling_independent(C, H, M, L, N, Q):
             outs.append(to_host(x))
     assert np.array_equal(outs[0], outs[1])
     ref = BK.stack_forward(x64, _f64(blocks), H, M, 2.0)
-    err = rel_l2(outs[0], ref)
-    print(f"stack rel L2 {err:.3e}", flush=True)
-    assert err <= BF16_TOL
+    assert_bf16_close(outs[0], ref, "stack", BF16_TOL)
 
 
 def test_decoding_the_mesh_reproduces_the_forward_and_query_points_match_the_oracle():
@@ -83,9 +81,7 @@ def test_decoding_the_mesh_reproduces_the_forward_and_query_points_match_the_ora
     b64 = _f64(blocks)
     Zs = BK.stack_states(x64, b64, H, M, 2.0)
     ref = BK.stack_decode(q64, b64, Zs, H, M, 2.0)
-    err = rel_l2(got, ref)
-    print(f"query decode rel L2 {err:.3e}", flush=True)
-    assert err <= BF16_TOL
+    assert_bf16_close(got, ref, "query decode", BF16_TOL)
 
 
 def test_decoding_from_injected_states():
@@ -107,9 +103,7 @@ def test_decoding_from_injected_states():
         got = to_host(q)
     Zs32 = [z.astype(np.float32).astype(np.float64) for z in Zs]
     ref = BK.stack_decode(q64, _f64(blocks), Zs32, H, M, 2.0)
-    err = rel_l2(got, ref)
-    print(f"injected-state decode rel L2 {err:.3e}", flush=True)
-    assert err <= BF16_TOL
+    assert_bf16_close(got, ref, "injected-state decode", BF16_TOL)
 
 
 def test_feedforward_half_matches_the_oracle_and_writes_the_next_layernorm():
@@ -131,7 +125,5 @@ def test_feedforward_half_matches_the_oracle_and_writes_the_next_layernorm():
     b = _f64(blocks)
     y = x64 + pa64
     ref = y + BK.mlp(BK.layer_norm(y, b[0]["ln2_g"], b[0]["ln2_b"]), b[0]["Wa"], b[0]["ba"], b[0]["Wb"], b[0]["bb"])
-    err = rel_l2(got, ref)
-    err_n = rel_l2(got_xn, BK.layer_norm(ref, b[1]["ln1_g"], b[1]["ln1_b"]))
-    print(f"feed-forward rel L2 {err:.3e}, next LN1 rel L2 {err_n:.3e}", flush=True)
-    assert err <= BF16_TOL and err_n <= BF16_TOL
+    assert_bf16_close(got, ref, "feed-forward", BF16_TOL)
+    assert_bf16_close(got_xn, BK.layer_norm(ref, b[1]["ln1_g"], b[1]["ln1_b"]), "next LN1", BF16_TOL)

@@ -12,7 +12,7 @@ The float64 oracle cannot run eight blocks over 1e7 points in test time, so:
 import numpy as np
 import pytest
 
-from gpu_helpers import banner, rel_l2, to_host
+from gpu_helpers import assert_bf16_close, banner, rel_l2, to_host
 from oracle import block as BK
 from ts3_synth import WORKLOADS, make_block_weights
 
@@ -91,6 +91,4 @@ def test_stack_decode_from_injected_states_at_10m_sampled(mesh):
         got = to_host(q)
     b64 = [{k: np.asarray(v, np.float64) for k, v in b.items()} for b in blocks]
     ref = BK.stack_decode(qs, b64, [z.astype(np.float64) for z in Zs], wl.H, wl.M, 1.0 / wl.tau)
-    err = rel_l2(got, ref)
-    print(f"sampled rel L2 {err:.3e}", flush=True)
-    assert err <= BF16_TOL
+    assert_bf16_close(got, ref, "sampled", BF16_TOL)

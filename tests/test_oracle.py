@@ -335,3 +335,20 @@ def test_planted_mistakes_are_caught(name, monkeypatch):
     monkeypatch.setattr(PA, fn_name, fn)
     monkeypatch.setattr(oracle, fn_name, fn, raising=False)
     assert not _pins_pass(), f"planted mistake '{name}' passed every pin"
+
+
+def test_pool_driver_equals_the_in_process_oracle_bitwise():
+    """oracle.pool only distributes tiles and chunks: its state and decoding
+    equal build_state / deslice bit for bit (same tile order, same zero start)."""
+    from oracle.pool import OraclePool
+    rng = np.random.default_rng(31)
+    C, H, M, N, tile = 32, 2, 16, 700, 96
+    x = rng.standard_normal((N, C)).astype(np.float32).astype(np.float64)
+    W = make_weights(C, H, M, C // H, seed=2, bias_seed=3)
+    ref = oracle.build_state(x, W, H, M, 1.7, tile=tile)
+    with OraclePool(2) as pool:
+        st = pool.state(x, W, H, M, 1.7, tile=tile)
+        out = pool.decode(x, W["W2"], W["b2"], st["Z"], W["b3"], H, M, 1.7, chunk=250)
+    for k in ("s_raw", "d", "s", "s1", "Z"):
+        assert np.array_equal(st[k], ref[k]), k
+    assert np.array_equal(out, oracle.deslice(x, W["W2"], W["b2"], ref["Z"], W["b3"], H, M, 1.7))
