@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -94,15 +95,21 @@ void launch_pass1(const void *x, int64_t n, int64_t span0, int32_t Q, int32_t ns
     }
 }
 
+// Compute units of the current device, looked up once per device.
 int device_cu_count() {
-    static int cus = 0;
-    if (!cus) {
-        int dev = 0;
-        if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
-            cus = 256;
+    static std::atomic<int> cache[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 256;
+    if (dev < 0 || dev >= 64) {
+        int c = 0;
+        return hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && c > 0 ? c : 256;
     }
-    return cus;
+    int c = cache[dev].load(std::memory_order_relaxed);
+    if (c <= 0) {
+        if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || c <= 0) c = 256;
+        cache[dev].store(c, std::memory_order_relaxed);
+    }
+    return c;
 }
 
 // Eight waves of 16 points (two per SIMD) measured faster than four of 32.
@@ -122,20 +129,18 @@ hipError_t launch_pass2(const void *x, int64_t n, int32_t H, const void *w2p, co
     } else if constexpr (sizeof(T) == 2 && C <= 128) {
         using WCfg = Pass2W8Cfg<T, C, M>;
         const size_t lds = WCfg::lds_bytes(H);
-        static size_t static_lds = SIZE_MAX;
-        if (static_lds == SIZE_MAX) {
+        // The kernel's static LDS is a property of its code (thread-safe init).
+        static const size_t static_lds = [] {
             hipFuncAttributes fa{};
-            static_lds = hipFuncGetAttributes(&fa, (const void *)k_deslice_w8<T, C, M>) == hipSuccess
-                             ? fa.sharedSizeBytes : PASS2_LDS_MAX;
-        }
-        static size_t dyn_set = 0;  // dynamic LDS limit granted so far
+            return hipFuncGetAttributes(&fa, (const void *)k_deslice_w8<T, C, M>) == hipSuccess
+                       ? fa.sharedSizeBytes : PASS2_LDS_MAX;
+        }();
         if (lds + static_lds <= PASS2_LDS_MAX) {
-            if (lds > dyn_set) {
-                if (hipFuncSetAttribute((const void *)k_deslice_w8<T, C, M>,
-                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
-                    return hipGetLastError();
-                dyn_set = lds;
-            }
+            // Granted on every call: the attribute may be per device, and the
+            // call costs microseconds against a launch of a million points.
+            if (hipFuncSetAttribute((const void *)k_deslice_w8<T, C, M>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                    (int)lds) != hipSuccess)
+                return hipGetLastError();
             // At most P2_MAX_ITERS blocks per workgroup and launch (the kernel
             // records slow-path blocks in a 64-bit mask); larger calls are
             // split, which changes no result: every point is decoded alone.
@@ -689,12 +694,7 @@ ts3_status ts3_layer_backward(ts3_state *st, const ts3_weights *w, const void *x
     // token side: ds_raw, dd and the Linear1 / attention / Linear3 gradients
     const size_t lds = (size_t)(2 * d.M * d.C + 10 * d.M * d.dh + 2 * d.M * d.M) * 4;
     if (lds > (size_t)ATTN_LDS_MAX) return fail(TS3_ERR_UNSUPPORTED, "token backward needs %zu bytes of LDS", lds);
-    static bool lds_set = false;
-    if (!lds_set) {
-        HIP_TRY(hipFuncSetAttribute((const void *)k_bw_token, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                    ATTN_LDS_MAX));
-        lds_set = true;
-    }
+    HIP_TRY(hipFuncSetAttribute((const void *)k_bw_token, hipFuncAttributeMaxDynamicSharedMemorySize, ATTN_LDS_MAX));
     hipLaunchKernelGGL(k_bw_token, dim3(d.H), dim3(256), lds, hs, st->s_raw, st->dsum, st->s, st->s1, st->bdZ,
                        w->W1, w->Wq, w->Wk, w->Wv, w->W3, d.C, d.H, d.M, d.dh, d.eps, st->bdsr, st->bdsT, st->bdd,
                        gr->dW1, gr->db1, gr->dWq, gr->dWk, gr->dWv, gr->dW3, gr->db3);
