@@ -173,6 +173,32 @@ ts3_status ts3_deslice(const ts3_state *st, const ts3_weights *w, const void *x_
 ts3_status ts3_layer_forward(ts3_state *st, const ts3_weights *w, const void *x, int64_t N,
                              int64_t tile, int64_t chunk, void *out, void *stream);
 
+/* ts3_layer_forward for callers that cannot allocate device memory: code
+ * under HIP graph capture, tight serving loops, and hosts that forbid
+ * allocation.  Same arguments and results as ts3_layer_forward (bitwise equal
+ * outputs for the same desc, weights, x, N and tile), but there is no state
+ * object: every buffer beyond x, out and the weights lives in one fixed
+ * 64 MiB device array inside the library.  Each GPU the library runs on holds
+ * its own copy of that array from the first call on that device until the
+ * process ends.  The call allocates and frees nothing (no hipMalloc, no
+ * stream or event creation).  All its work runs on `stream`; tiles run one
+ * after another (no second stream).
+ *  - Scratch needed: the span partials of one tile, ceil(tile / group_span) *
+ *    H*M*(C+1) floats, plus the run sums of the mesh, ceil(ceil(N /
+ *    group_span) / 64) * H*M*(C+1) floats (doubles with TS3_ACCUM_FP64), plus
+ *    under 1 MiB of token-side buffers.  At C=128, H*M=512, group_span 15,625
+ *    and 1M-point tiles that is about 44 MB for 100M points.  A call that needs
+ *    more than 64 MiB returns TS3_ERR_INVALID_ARG before enqueuing anything.
+ *  - Calls that overlap on one GPU (from several threads or streams) share the
+ *    array and race: serialise them.  The array keeps the last call's
+ *    contents; every region a call reads is written by that call first.
+ *  - desc is validated as for ts3_state_create (max_points is not used).
+ *  - N = 0 is valid: only the token-side work of an empty mesh runs and out
+ *    is not touched.
+ * The cached state is not retained after the call returns. */
+ts3_status ts3_layer_forward_noalloc(const ts3_desc *desc, const ts3_weights *w, const void *x, int64_t N,
+                                     int64_t tile, int64_t chunk, void *out, void *stream);
+
 /* Backward of the layer (section 3.2: the training loop checkpoints every
  * tile, so the slice weights are recomputed tile by tile, never stored).
  * Given the output gradient g = dL/dx_out [N, C], writes dx = dL/dx [N, C]

@@ -55,6 +55,8 @@ SIGNATURES = {
     "ts3_token_attention": (ct.c_int, [_P, ct.POINTER(Weights), _P]),
     "ts3_deslice": (ct.c_int, [_P, ct.POINTER(Weights), _P, ct.c_int64, _P, _P]),
     "ts3_layer_forward": (ct.c_int, [_P, ct.POINTER(Weights), _P, ct.c_int64, ct.c_int64, ct.c_int64, _P, _P]),
+    "ts3_layer_forward_noalloc": (ct.c_int, [ct.POINTER(Desc), ct.POINTER(Weights), _P, ct.c_int64, ct.c_int64,
+                                             ct.c_int64, _P, _P]),
     "ts3_layer_backward": (ct.c_int, [_P, ct.POINTER(Weights), _P, _P, ct.c_int64, ct.c_int64, _P,
                                       ct.POINTER(Grads), _P]),
     "ts3_state_get": (ct.c_int, [_P, ct.c_int32, _P, ct.c_int64, _P]),

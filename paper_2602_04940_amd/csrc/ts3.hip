@@ -5,6 +5,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <mutex>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -775,6 +776,178 @@ ts3_status ts3_state_set(ts3_state *st, const ts3_weights *w, int32_t which, con
     HIP_TRY(hipStreamSynchronize(hs));
     st->phase = PH_ATTEND;
     return TS3_OK;
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Layer forward without allocation (ts3_layer_forward_noalloc).  Every buffer
+// the layer needs beyond x, out and the weights lives in one file-scope device
+// array.  Its device address is looked up once per device; host code uses only
+// that address, never the array's name, which in host code is a stand-in and
+// not a device pointer.
+namespace {
+
+constexpr size_t SCRATCH_BYTES = size_t(64) << 20;
+constexpr int SCRATCH_MAX_DEVICES = 64;
+static __device__ __align__(256) unsigned char scratch[SCRATCH_BYTES];
+
+std::once_flag g_scratch_once[SCRATCH_MAX_DEVICES];
+void *g_scratch_ptr[SCRATCH_MAX_DEVICES];
+hipError_t g_scratch_err[SCRATCH_MAX_DEVICES];
+
+// The current device's copy of the array (each device holds its own).
+ts3_status scratch_base(void **out) {
+    int dev = 0;
+    HIP_TRY(hipGetDevice(&dev));
+    if (dev < 0 || dev >= SCRATCH_MAX_DEVICES)
+        return fail(TS3_ERR_UNSUPPORTED, "device %d: the no-allocation path serves devices 0..%d", dev,
+                    SCRATCH_MAX_DEVICES - 1);
+    std::call_once(g_scratch_once[dev], [dev] {
+        g_scratch_err[dev] = hipGetSymbolAddress(&g_scratch_ptr[dev], HIP_SYMBOL(scratch));
+    });
+    if (g_scratch_err[dev] != hipSuccess)
+        return fail(TS3_ERR_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev,
+                    hipGetErrorString(g_scratch_err[dev]));
+    *out = g_scratch_ptr[dev];
+    return TS3_OK;
+}
+
+// Byte layout of the scratch array for one call (each region 256-aligned).
+struct ScratchLayout {
+    size_t partials, runs, s_raw, dsum, s, s1, Z, b2s, b3, w2p, zp, total;
+};
+
+ScratchLayout scratch_layout(const ts3_desc &d, int64_t N, int64_t tile) {
+    auto up = [](size_t b) { return (b + 255) & ~size_t(255); };
+    const int64_t HM = (int64_t)d.H * d.M;
+    const int64_t E = HM * (d.C + 1);
+    const int64_t Q = d.group_span;
+    const int64_t tile_spans = (std::min<int64_t>(tile, std::max<int64_t>(N, 1)) + Q - 1) / Q;
+    // An empty mesh still folds one (zero) span.
+    const int64_t nrun = (std::max<int64_t>((N + Q - 1) / Q, 1) + FOLD - 1) / FOLD;
+    const int esize = d.io_dtype == TS3_BF16 ? 2 : 4;
+    const int KM = d.M >= 32 ? d.M / 32 : 1;
+    ScratchLayout L{};
+    size_t at = 0;
+    auto take = [&](size_t &field, size_t bytes) { field = at; at += up(bytes); };
+    take(L.partials, (size_t)(tile_spans * E) * 4);
+    take(L.runs, (size_t)(nrun * E) * (d.accum == TS3_ACCUM_FP64 ? 8 : 4));
+    take(L.s_raw, (size_t)(HM * d.C) * 4);
+    take(L.dsum, (size_t)HM * 4);
+    take(L.s, (size_t)(HM * d.dh) * 4);
+    take(L.s1, (size_t)(HM * d.dh) * 4);
+    take(L.Z, (size_t)(HM * d.C) * 4);
+    take(L.b2s, (size_t)HM * 4);
+    take(L.b3, (size_t)d.C * 4);
+    take(L.w2p, (size_t)d.H * (d.M / 16) * (d.C / 32) * 512 * esize);
+    take(L.zp, (size_t)d.H * (d.C / 16) * KM * 512 * esize);
+    L.total = at;
+    return L;
+}
+
+template <typename T>
+void fold_tile(const float *partials, int64_t E, int64_t g0, int64_t ns, void *runs, hipStream_t hs) {
+    const int64_t r_first = g0 / FOLD, r_last = (g0 + ns - 1) / FOLD;
+    hipLaunchKernelGGL(k_fold_runs_tile<T>, dim3((unsigned)((E + 255) / 256), (unsigned)(r_last - r_first + 1)),
+                       dim3(256), 0, hs, partials, E, g0, ns, (T *)runs);
+}
+
+}  // namespace
+
+extern "C" {
+
+ts3_status ts3_layer_forward_noalloc(const ts3_desc *desc, const ts3_weights *w, const void *x, int64_t N,
+                                     int64_t tile, int64_t chunk, void *out, void *stream) {
+    ts3_status s = check_desc(desc);
+    if (s != TS3_OK) return s;
+    s = check_weights_w2(w);
+    if (s != TS3_OK) return s;
+    if (!w->W1 || !w->Wq || !w->Wk || !w->Wv || !w->W3)
+        return fail(TS3_ERR_INVALID_ARG, "W1, Wq, Wk, Wv or W3 is NULL");
+    const ts3_desc &d = *desc;
+    if (N < 0 || tile <= 0 || chunk <= 0) return fail(TS3_ERR_INVALID_ARG, "N >= 0, tile > 0, chunk > 0 required");
+    if (tile % d.group_span != 0)
+        return fail(TS3_ERR_INVALID_ARG, "tile %lld is not a multiple of group_span %lld", (long long)tile,
+                    (long long)d.group_span);
+    if (N > 0 && (!x || !out)) return fail(TS3_ERR_INVALID_ARG, "x or out is NULL");
+    if (((uintptr_t)x & 15) || ((uintptr_t)out & 15))
+        return fail(TS3_ERR_INVALID_ARG, "x and out must be 16-byte aligned");
+    if (N > ((int64_t)INT32_MAX) * 64) return fail(TS3_ERR_INVALID_ARG, "N too large");
+    const ScratchLayout lay = scratch_layout(d, N, tile);
+    if (lay.total > SCRATCH_BYTES)
+        return fail(TS3_ERR_INVALID_ARG,
+                    "this call needs %llu bytes of scratch (span partials of one %lld-point tile and the run sums "
+                    "of %lld points); the fixed maximum is %llu bytes: use fewer points, smaller tiles or a "
+                    "larger group_span, or ts3_layer_forward",
+                    (unsigned long long)lay.total, (long long)tile, (long long)N,
+                    (unsigned long long)SCRATCH_BYTES);
+    void *base = nullptr;
+    s = scratch_base(&base);
+    if (s != TS3_OK) return s;
+    unsigned char *b = (unsigned char *)base;
+    // A state on the host stack whose device buffers are regions of the array;
+    // it owns nothing and is never freed.
+    ts3_state st;
+    st.desc = d;
+    find_kernels(d.io_dtype, d.C, d.M, &st.k);
+    st.esize = d.io_dtype == TS3_BF16 ? 2 : 4;
+    st.E = (int64_t)d.H * d.M * (d.C + 1);
+    st.partials = (float *)(b + lay.partials);
+    st.runs = (float *)(b + lay.runs);
+    st.s_raw = (float *)(b + lay.s_raw);
+    st.dsum = (float *)(b + lay.dsum);
+    st.s = (float *)(b + lay.s);
+    st.s1 = (float *)(b + lay.s1);
+    st.Z = (float *)(b + lay.Z);
+    st.b2s = (float *)(b + lay.b2s);
+    st.b3 = (float *)(b + lay.b3);
+    st.w2p = b + lay.w2p;
+    st.zp = b + lay.zp;
+    hipStream_t hs = (hipStream_t)stream;
+    const int64_t Q = d.group_span;
+    const int64_t E = st.E;
+    const int64_t nspan = std::max<int64_t>((N + Q - 1) / Q, 1);
+    const int64_t nrun = (nspan + FOLD - 1) / FOLD;
+    s = prep_w2(&st, w, hs);
+    if (s != TS3_OK) return s;
+    if (N == 0) {  // an empty mesh: the one span is zero
+        hipLaunchKernelGGL(k_zero, dim3((unsigned)((E + 255) / 256)), dim3(256), 0, hs, st.partials, E);
+        LAUNCH_CHECK("zero span");
+        if (d.accum == TS3_ACCUM_FP64) fold_tile<double>(st.partials, E, 0, 1, st.runs, hs);
+        else fold_tile<float>(st.partials, E, 0, 1, st.runs, hs);
+        LAUNCH_CHECK("fold");
+    }
+    // Pass 1 tile by tile on the caller's stream: the tile's spans go to the
+    // start of the partial region, then into their runs.
+    for (int64_t t0 = 0; t0 < N; t0 += tile) {
+        const int64_t nt = std::min(tile, N - t0);
+        const int64_t ns = (nt + Q - 1) / Q;
+        st.k.pass1((const char *)x + t0 * d.C * st.esize, nt, 0, (int32_t)Q, (int32_t)ns, d.H, st.w2p, st.b2s,
+                   st.partials, hs);
+        LAUNCH_CHECK("slice_accumulate");
+        if (d.accum == TS3_ACCUM_FP64) fold_tile<double>(st.partials, E, t0 / Q, ns, st.runs, hs);
+        else fold_tile<float>(st.partials, E, t0 / Q, ns, st.runs, hs);
+        LAUNCH_CHECK("fold");
+    }
+    const unsigned gx = (unsigned)((E + 255) / 256);
+    if (d.accum == TS3_ACCUM_FP64)
+        hipLaunchKernelGGL(k_fold_final<double>, dim3(gx), dim3(256), 0, hs, (const double *)st.runs, E, nrun, d.C,
+                           st.s_raw, st.dsum);
+    else
+        hipLaunchKernelGGL(k_fold_final<float>, dim3(gx), dim3(256), 0, hs, (const float *)st.runs, E, nrun, d.C,
+                           st.s_raw, st.dsum);
+    LAUNCH_CHECK("fold_final");
+    hipLaunchKernelGGL(k_finalize, dim3(d.H), dim3(256), (size_t)d.M * d.C * 4, hs, st.s_raw, st.dsum, w->W1,
+                       w->b1, d.C, d.H, d.M, d.dh, d.eps, st.s);
+    LAUNCH_CHECK("finalize");
+    st.phase = PH_FINAL;
+    s = ts3_token_attention(&st, w, stream);
+    if (s != TS3_OK) return s;
+    for (int64_t c0 = 0; s == TS3_OK && c0 < N; c0 += chunk)
+        s = ts3_deslice(&st, w, (const char *)x + c0 * d.C * st.esize, std::min(chunk, N - c0),
+                        (char *)out + c0 * d.C * st.esize, stream);
+    return s;
 }
 
 }  // extern "C"

@@ -83,6 +83,25 @@ __global__ void k_fold_runs(const float *__restrict__ partials, int64_t E, int64
     runs[run * E + e] = acc;
 }
 
+// The same fold taken one tile at a time: the tile's spans [g0, g0 + ns)
+// (partials[0 .. ns) of this launch) are added to the runs they fall in.  A
+// run starting inside the tile starts from zero, one begun by an earlier tile
+// continues from its stored sum; each run is thus the same sequential sum,
+// in span order, as k_fold_runs forms, and holds the same bits.
+template <typename T>
+__global__ void k_fold_runs_tile(const float *__restrict__ partials, int64_t E, int64_t g0, int64_t ns,
+                                 T *__restrict__ runs) {
+    const int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    const int64_t run = g0 / FOLD + blockIdx.y;
+    if (e >= E) return;
+    const int64_t r0 = run * FOLD;
+    const int64_t s0 = r0 > g0 ? r0 : g0;
+    const int64_t s1 = r0 + FOLD < g0 + ns ? r0 + FOLD : g0 + ns;
+    T acc = s0 == r0 ? (T)0 : runs[run * E + e];
+    for (int64_t s = s0; s < s1; ++s) acc += (T)partials[(s - g0) * E + e];
+    runs[run * E + e] = acc;
+}
+
 template <typename T>
 __global__ void k_fold_final(const T *__restrict__ runs, int64_t E, int64_t nrun, int C, float *__restrict__ s_raw,
                              float *__restrict__ dsum) {

@@ -168,5 +168,22 @@ class PhysicsAttention:
                                       _stream()), "ts3_state_set")
 
 
+def layer_forward_noalloc(C, H, M, w: LayerWeights, x, tile: int, chunk: int, out, dh=None, temperature=0.5,
+                          dtype="bf16", group_span=32768, eps=0.0, accum="fp32"):
+    """ts3_layer_forward_noalloc: the whole layer over x into the preallocated
+    out, with the library's fixed scratch array instead of a state object."""
+    code, torch_dtype = _DTYPES[dtype]
+    dh = C // H if dh is None else dh
+    acc = {"fp32": L.TS3_ACCUM_FP32, "fp64": L.TS3_ACCUM_FP64}[accum]
+    for t, name in ((x, "x"), (out, "out")):
+        if not (t.is_cuda and t.dtype == torch_dtype and t.is_contiguous() and t.dim() == 2 and t.shape[1] == C):
+            raise ValueError(f"{name} must be a contiguous cuda {torch_dtype} tensor [n, {C}]")
+    desc = L.Desc(C=C, H=H, M=M, dh=dh, temperature=temperature, eps=eps, io_dtype=code, accum=acc,
+                  group_span=group_span, max_points=x.shape[0])
+    L.check(L.lib().ts3_layer_forward_noalloc(ct.byref(desc), w.ref(), _ptr(x), x.shape[0], tile, chunk, _ptr(out),
+                                              _stream()), "ts3_layer_forward_noalloc")
+    return out
+
+
 def inv_tau_of(temperature: float) -> float:
     return 0.0 if math.isinf(temperature) else 1.0 / temperature

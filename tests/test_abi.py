@@ -126,3 +126,18 @@ def test_package_import_loads_nothing_and_product_has_no_oracle_dependency():
     r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, capture_output=True, text=True, timeout=120)
     assert r.returncode == 0, r.stderr
     assert r.stdout.strip() == "[]", r.stdout
+
+
+def test_noalloc_rejects_a_call_beyond_its_fixed_scratch_before_any_device_call():
+    """ts3_layer_forward_noalloc checks its scratch need on the host: 1e9 points
+    in spans of 1,024 need ~1 GB of run sums, far past the 64 MiB array."""
+    lib = L.lib()
+    d = _desc(group_span=1024, max_points=0)
+    w = L.Weights(*([0x1000] * 9))
+    fake = ct.c_void_p(0x10000)  # aligned, never dereferenced: the call fails before touching it
+    st = lib.ts3_layer_forward_noalloc(ct.byref(d), ct.byref(w), fake, 10 ** 9, 1 << 20, 1 << 20, fake, None)
+    assert st == L.TS3_ERR_INVALID_ARG
+    assert b"scratch" in lib.ts3_last_error()
+    d2 = _desc(group_span=1000)
+    assert lib.ts3_layer_forward_noalloc(ct.byref(d2), ct.byref(w), fake, 4096, 1024, 1024, fake,
+                                         None) == L.TS3_ERR_INVALID_ARG  # tile not a multiple of the span
