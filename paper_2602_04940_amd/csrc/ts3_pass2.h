@@ -367,24 +367,27 @@ __global__ __launch_bounds__(512, 1) void k_deslice_w8(const T *__restrict__ x, 
                 }
                 ok = !__any(!okk) && ok;
             }
-            // Z fragments of channel tile ct+1 are read while tile ct's MFMAs run.
+            // Decode with the K steps outermost: the MFMAs into one output
+            // accumulator are CT steps apart, so the matrix core always has
+            // independent work (on gfx950 an MFMA that depends on the one
+            // before it issues at half rate); the Z fragment of step q+2 is
+            // read while step q's MFMAs run.
             {
                 const T *zl = zs + (size_t)cur * Cfg::STAGE_ELEMS + lane * 8;
-                Frag<T> a[2][KM];
+                constexpr int NQ = KM * CT, DZ = 2;
+                auto zfrag = [&](int q) { return zl + ((q % CT) * KM + q / CT) * 512; };
+                Frag<T> a[4];
 #pragma unroll
-                for (int km = 0; km < KM; ++km) load8(a[0][km], zl + km * 512);
+                for (int q = 0; q < DZ; ++q) load8(a[q], zfrag(q));
 #pragma unroll
-                for (int ct = 0; ct < CT; ++ct) {
+                for (int q = 0; q < NQ; ++q) {
+                    const int km = q / CT, ct = q % CT;
                     __builtin_amdgcn_sched_barrier(0);
-                    if (ct + 1 < CT)
+                    if (q + DZ < NQ) load8(a[(q + DZ) & 3], zfrag(q + DZ));
 #pragma unroll
-                        for (int km = 0; km < KM; ++km) load8(a[(ct + 1) & 1][km], zl + ((ct + 1) * KM + km) * 512);
-#pragma unroll
-                    for (int km = 0; km < KM; ++km)
-#pragma unroll
-                        for (int pt = 0; pt < PT; ++pt) mma(O[ct][pt], a[ct & 1][km], wf[pt][km]);
-                    if (ct + 1 < CT) __builtin_amdgcn_sched_group_barrier(0x100, KM, 0);
-                    __builtin_amdgcn_sched_group_barrier(0x008, KM * PT, 0);
+                    for (int pt = 0; pt < PT; ++pt) mma(O[ct][pt], a[q & 3], wf[pt][km]);
+                    if (q + DZ < NQ) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x008, PT, 0);
                 }
                 __builtin_amdgcn_sched_barrier(0);
             }
