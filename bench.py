@@ -13,8 +13,9 @@ bounded sample.  Prints one JSON line on stdout; progress goes to stderr.
 
 --backward times a float32 training step of the layer instead (forward, then
 the backward with the slice weights recomputed per tile) on 2M volume points
-(C=128, H=8, M=64, 1M-point tiles), with the backward's roofline against the
-float32 matrix peak and the float64 backward oracle as the CPU baseline.
+drawn by seed without replacement from a 160M-point volume mesh (C=128, H=8,
+M=64, 1M-point tiles), with the backward's roofline against the float32 matrix
+peak and the float64 backward oracle as the CPU baseline.
 
 --stack times the 8-block pre-norm Transolver stack (Physics-Attention plus a
 4C feed-forward network per block) on a 10M-point car surface (C=256, H=8,
@@ -104,10 +105,11 @@ def pmc_driver(points: int, workloads=("layer",)):
         del x
         log("pmc driver: stack done")
     if "backward" in workloads:
+        from ts3_synth.workloads import subset_indices
         wl = WORKLOADS["volume_2m_fp32"]
         n = 1_000_000
         x = torch.empty((n, wl.C), device="cuda", dtype=torch.float32)
-        DeviceVolume(wl.seed, wl.C, dtype=torch.float32).fill(x)
+        DeviceVolume(wl.seed, wl.C, dtype=torch.float32).gather(x, subset_indices(wl)[:n], wl.source_N)
         gen = torch.Generator(device="cuda")
         gen.manual_seed(wl.seed + 1000)
         g = torch.randn((n, wl.C), device="cuda", dtype=torch.float32, generator=gen)
@@ -346,7 +348,7 @@ def cpu_baseline_backward(x_dev, g_dev, W, wl, sample):
     threads = min(max([p.get("num_threads", 1) for p in threadpool_info()] + [1]), len(os.sched_getaffinity(0)))
     return {"value": sample / dt, "unit": "points/s", "cores": threads, "kind": "oracle",
             "sample": f"layer forward state + backward (all gradients) in float64 numpy on the first {sample} "
-                      f"points of the mesh: {dt:.1f} s"}
+                      f"points of the training subset: {dt:.1f} s"}
 
 
 def bench_backward(args):
@@ -359,13 +361,16 @@ def bench_backward(args):
     from ts3_synth import WORKLOADS, make_weights
     from ts3_synth.device_gen import DeviceVolume
 
+    from ts3_synth.workloads import subset_indices
     wl = WORKLOADS["volume_2m_fp32"]
     N = args.points or wl.N
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    log(f"generating {N} volume points on the device (C={wl.C}, fp32) and an output gradient")
+    log(f"drawing {N} of the {wl.source_N} points of the volume mesh (seed {wl.subset_seed}) on the device "
+        f"(C={wl.C}, fp32), and an output gradient")
     x = torch.empty((N, wl.C), device=dev, dtype=torch.float32)
-    DeviceVolume(wl.seed, wl.C, dev, dtype=torch.float32).fill(x)
+    DeviceVolume(wl.seed, wl.C, dev, dtype=torch.float32).gather(
+        x, subset_indices(wl)[:N], wl.source_N, progress=lambda k: log(f"  mesh chunk {k}/{wl.source_N // 1_000_000}"))
     gen = torch.Generator(device=dev)
     gen.manual_seed(wl.seed + 1000)
     g = torch.randn((N, wl.C), device=dev, dtype=torch.float32, generator=gen)
@@ -418,8 +423,9 @@ def bench_backward(args):
         "metric": METRIC_BW, "value": N / (ms * 1e-3), "unit": "points/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
-        "data": "synthetic: seeded volume mesh (box minus car-like body), Fourier features, device-generated; "
-                "output gradient N(0,1)",
+        "data": f"synthetic: {N} points drawn uniformly without replacement (seed {wl.subset_seed}) from a "
+                f"{wl.source_N}-point seeded volume mesh (box minus car-like body), Fourier features, "
+                "device-generated; output gradient N(0,1)",
         "config": {"workload": wl.name, "N": N, "C": wl.C, "H": wl.H, "M": wl.M, "dh": wl.dh, "tau": wl.tau,
                    "tile": wl.tile, "chunk": wl.chunk, "group_span": wl.group_span},
         "passes_ms": {"forward": round(t_fw, 3), "backward": round(t_bw, 3)},

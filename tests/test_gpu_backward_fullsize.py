@@ -1,10 +1,12 @@
-"""The layer backward at the training workload's full size: 2M volume points,
-C=128, H=8, M=64, float32, 1M-point tiles and group span 15,625 (the launch
-configuration ``bench.py --backward`` times).
+"""The layer backward at the training workload's full size: 2M points drawn by
+seed without replacement from a 160M-point volume mesh (section 3.2's training
+on subsets of the full mesh), C=128, H=8, M=64, float32, 1M-point tiles and
+group span 15,625 (the launch configuration ``bench.py --backward`` times).
 
+The drawn rows are first checked to be the mesh's rows at the drawn indices.
 The float64 backward oracle needs minutes for 2M points, so the full size is
 checked through properties that hold at any size, and the oracle itself is
-compared on the first 40,000 points of the same mesh (two spans and a ragged
+compared on the first 40,000 points of the same subset (two spans and a ragged
 third, the mesh's own feature distribution):
   * reruns, and untiled (one 2M-point tile) runs, are bitwise equal;
   * scaling g by 2 scales every gradient by exactly 2 (the backward is linear
@@ -32,10 +34,11 @@ NAMES = ("dW2", "db2", "dW1", "db1", "dWq", "dWk", "dWv", "dW3", "db3")
 def problem():
     import torch
     from ts3_synth.device_gen import DeviceVolume
+    from ts3_synth.workloads import subset_indices
     wl = WORKLOADS["volume_2m_fp32"]
-    banner(f"{wl.name}: generating {wl.N} points and an output gradient on the device")
+    banner(f"{wl.name}: drawing {wl.N} of {wl.source_N} mesh points and an output gradient on the device")
     x = torch.empty((wl.N, wl.C), device="cuda", dtype=torch.float32)
-    DeviceVolume(wl.seed, wl.C, dtype=torch.float32).fill(x)
+    DeviceVolume(wl.seed, wl.C, dtype=torch.float32).gather(x, subset_indices(wl), wl.source_N)
     gen = torch.Generator(device="cuda")
     gen.manual_seed(wl.seed + 1000)
     g = torch.randn((wl.N, wl.C), device="cuda", dtype=torch.float32, generator=gen)
@@ -44,6 +47,23 @@ def problem():
     yield wl, x, g, W
     del x, g
     torch.cuda.empty_cache()
+
+
+def test_the_drawn_rows_are_the_mesh_rows_at_the_drawn_indices():
+    """gather() on the device against fill() of the same mesh: a 5M-point
+    volume mesh, 40,000 indices drawn as the training subset is, bitwise."""
+    import torch
+    from ts3_synth.device_gen import DeviceVolume
+    wl = WORKLOADS["volume_2m_fp32"]
+    source = 5_000_000
+    idx = np.sort(np.random.default_rng(wl.subset_seed).choice(source, 40_000, replace=False))
+    banner(f"gather of {len(idx)} rows of a {source}-point mesh vs fill")
+    gen = DeviceVolume(wl.seed, wl.C, dtype=torch.float32)
+    full = torch.empty((source, wl.C), device="cuda", dtype=torch.float32)
+    gen.fill(full)
+    x = torch.empty((len(idx), wl.C), device="cuda", dtype=torch.float32)
+    gen.gather(x, idx, source)
+    assert torch.equal(x, full[torch.from_numpy(idx).cuda()])
 
 
 def _layer(wl, N):
@@ -145,7 +165,7 @@ def test_gradient_matches_central_differences_of_the_forward_at_2m(problem, whic
     assert rel <= 1e-2
 
 
-def test_backward_matches_oracle_on_the_first_40k_points_of_the_mesh(problem):
+def test_backward_matches_oracle_on_the_first_40k_points_of_the_subset(problem):
     wl, x, g, W = problem
     N = 40_000
     xs, gs = x[:N].contiguous(), g[:N].contiguous()

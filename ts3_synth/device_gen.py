@@ -75,6 +75,31 @@ class DeviceVolume:
         return x
 
 
+    def gather(self, x: torch.Tensor, indices, source_N: int, progress=None):
+        """Write rows ``indices`` (sorted, distinct, < source_N) of a source_N-point
+        mesh into x [len(indices), C]: every chunk holding a drawn row is
+        generated with the same calls ``fill`` makes for that mesh and the drawn
+        rows are selected from it, so they are the rows ``fill`` writes at those
+        positions."""
+        idx = np.asarray(indices, dtype=np.int64)
+        if len(idx) != x.shape[0]:
+            raise ValueError("x must have one row per index")
+        if len(idx) and ((np.diff(idx) <= 0).any() or idx[0] < 0 or idx[-1] >= source_N):
+            raise ValueError("indices must be sorted, distinct and in [0, source_N)")
+        chunks = idx // G.CHUNK
+        bounds = np.searchsorted(chunks, np.arange(chunks[-1] + 2)) if len(idx) else np.zeros(1, np.int64)
+        for k in range(len(bounds) - 1):
+            a, b = int(bounds[k]), int(bounds[k + 1])
+            if a == b:
+                continue
+            local = torch.from_numpy(idx[a:b] - k * G.CHUNK).to(self.device)
+            n = min(G.CHUNK, source_N - k * G.CHUNK)
+            x[a:b] = self.features(self.points(k, n))[local]
+            if progress and (k % 20 == 19 or b == len(idx)):
+                progress(k + 1)
+        return x
+
+
 class DeviceSurface(DeviceVolume):
     """Points on the car-like body's surface (uniform in direction, the host
     recipe of ``geometry.car_surface_chunk``), features over the body's padded

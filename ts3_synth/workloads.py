@@ -31,6 +31,8 @@ class Workload:
     tile: int
     chunk: int
     group_span: int
+    source_N: int = 0      # > 0: the N points are a seeded draw from a mesh of this many
+    subset_seed: int = 0   # seed of that draw (numpy default_rng)
 
 
 WORKLOADS = {
@@ -44,10 +46,11 @@ WORKLOADS = {
     "car_10m_bf16": Workload("car_10m_bf16", "car_surface", 3, 10_000_000, 256, 8, 64, 32, 0.5,
                              "bf16", 1_000_000, 1_000_000, 31_250),
     # a training step of one layer (forward and backward, float32) on 2M volume
-    # points: a uniform sample of the volume mesh (its points are i.i.d.
-    # uniform in the domain, so the first 2M points are such a sample)
+    # points drawn uniformly without replacement from a 160M-point volume mesh
+    # (the geometry-amortized training of section 3.2 samples subsets of the
+    # full mesh)
     "volume_2m_fp32": Workload("volume_2m_fp32", "volume", 5, 2_000_000, 128, 8, 64, 16, 0.5,
-                               "fp32", 1_000_000, 1_000_000, 15_625),
+                               "fp32", 1_000_000, 1_000_000, 15_625, source_N=160_000_000, subset_seed=6),
     # cached-state inference over 100M volume points, 1M-point tiles and chunks
     "volume_100m_bf16": Workload("volume_100m_bf16", "volume", 4, 100_000_000, 128, 8, 64, 16, 0.5,
                                  "bf16", 1_000_000, 1_000_000, 15_625),
@@ -99,6 +102,15 @@ def features(w: Workload, start: int, n: int) -> np.ndarray:
         out[pos - start:pos - start + take] = full[off:off + take]
         pos += take
     return out
+
+
+def subset_indices(w: Workload) -> np.ndarray:
+    """Mesh rows of a drawn workload: w.N indices drawn uniformly without
+    replacement from range(w.source_N) by numpy's default_rng(w.subset_seed),
+    sorted ascending (so the subset keeps the mesh's order)."""
+    if not w.source_N:
+        return np.arange(w.N, dtype=np.int64)
+    return np.sort(np.random.default_rng(w.subset_seed).choice(w.source_N, w.N, replace=False)).astype(np.int64)
 
 
 def small_features(w: Workload, n: int) -> np.ndarray:
