@@ -246,7 +246,12 @@ __global__ __launch_bounds__(512, 1) void k_slice_accumulate_pc(
                          "+v"(ws13));
             const int valid = block_valid(j);
             f32x4 L[MT][2];
+            // The producer's logits MFMAs go first on the SIMD's matrix core
+            // (the consumer's contraction fills the softmax that follows):
+            // measured 2% faster than equal priorities.
+            __builtin_amdgcn_s_setprio(2);
             logits(slot, L);
+            __builtin_amdgcn_s_setprio(0);
             float inv[2];
             bool ok = true;
 #pragma unroll
