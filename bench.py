@@ -241,6 +241,44 @@ def summarize_counters(sq_dir: str, fetch_dir: str, write_dir: str, command: str
     return out
 
 
+def summarize_trace(trace_dir: str, command: str, out_path: str, title: str):
+    """Kernel-trace summary (text) of one rocprofv3 --kernel-trace run: every
+    kernel's calls and durations, and separately the launches that overlapped
+    no other launch of this library (single-stream launch durations)."""
+    import csv
+    import glob
+
+    f = glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True)
+    if not f:
+        raise SystemExit(f"no kernel_trace.csv under {trace_dir}")
+    rows = [r for r in csv.DictReader(open(f[0])) if "ts3::" in r["Kernel_Name"]]
+    ev = sorted((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), r["Kernel_Name"]) for r in rows)
+
+    def table(items):
+        agg = {}
+        for a, b, k in items:
+            agg.setdefault(k, []).append((b - a) * 1e-3)
+        out = [f"{'kernel':62s} {'calls':>6s} {'avg_us':>10s} {'min_us':>10s} {'max_us':>10s}"]
+        for k, v in sorted(agg.items(), key=lambda kv: -sum(kv[1])):
+            out.append(f"{k[:62]:62s} {len(v):6d} {sum(v) / len(v):10.1f} {min(v):10.1f} {max(v):10.1f}")
+        return out
+
+    alone = []
+    for i, (a, b, k) in enumerate(ev):
+        prev_end = max((e[1] for e in ev[max(0, i - 8):i]), default=0)
+        nxt = ev[i + 1][0] if i + 1 < len(ev) else b + 1
+        if a >= prev_end and nxt >= b:
+            alone.append((a, b, k))
+    lines = [title, f"command: {command}", "", "All launches:"] + table(ev)
+    lines += ["", "Launches that overlapped no other launch of the library:"] + table(alone)
+    lines += ["", f"kernel source hash {kernel_source_hash()}"]
+    text = "\n".join(lines) + "\n"
+    os.makedirs(os.path.dirname(out_path) or ".", exist_ok=True)
+    with open(out_path, "w") as fh:
+        fh.write(text)
+    print(text)
+
+
 def summarize_traffic(fetch_dir: str, write_dir: str, command: str):
     """profiles/traffic.json from two rocprofv3 --pmc runs of --pmc-driver."""
     import csv
@@ -585,6 +623,8 @@ def main():
     ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="write profiles/traffic.json from two --pmc runs of --pmc-driver")
     ap.add_argument("--command", default="", help="command line recorded with --summarize-traffic")
+    ap.add_argument("--summarize-trace", nargs=3, metavar=("TRACE_DIR", "OUT", "TITLE"),
+                    help="kernel-trace summary of a rocprofv3 --kernel-trace run")
     ap.add_argument("--backward", action="store_true",
                     help="time a float32 training step (forward + backward) on 2M points instead")
     ap.add_argument("--cpu-sample-backward", type=int, default=100_000)
@@ -596,6 +636,9 @@ def main():
     args = ap.parse_args()
     if args.summarize_traffic:
         summarize_traffic(*args.summarize_traffic, args.command)
+        return
+    if args.summarize_trace:
+        summarize_trace(args.summarize_trace[0], args.command, args.summarize_trace[1], args.summarize_trace[2])
         return
     if args.summarize_counters:
         summarize_counters(*args.summarize_counters[:3], args.command, args.summarize_counters[3])
