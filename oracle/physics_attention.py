@@ -17,10 +17,13 @@ that head's M tokens with scale 1/sqrt(dh).
 Two forms are given and must agree (the paper states the reordering is exact,
 section 3.2, "Faster slice and deslice"):
   * ``layer_forward_orig``: project then slice, Eq. (1)-(2);
-  * ``layer_forward_fast``: slice then project, Eq. (3), tiled as in Eq. (4)
-    and Algorithm 1, with the cached state decoded as in Eq. (5).
-The fast form is also exposed step by step (``slice_accumulate`` ...
-``deslice``) so each GPU entry point has a matching oracle step.
+  * ``layer_forward_fast``: slice then project: the state of Eq. (3) in closed
+    form over the whole mesh, then each point decoded by Eq. (5).  Eq. (4)'s
+    additivity over parts of the mesh is what tiling relies on; it is a pinned
+    property here, not the way the state is defined.
+The reordered form is also exposed in pieces (``slice_accumulate`` for any
+part of the mesh, ``token_side`` ... ``deslice``) so each GPU entry point has
+a matching oracle step.
 
 Parity pins: every function here is checked in ``tests/test_oracle.py``
 against brute-force loops, closed forms (M = 1, 1/tau = 0, one-hot slices),
@@ -134,34 +137,38 @@ def deslice(x_chunk, W2, b2, Z, b3, H: int, M: int, inv_tau: float) -> np.ndarra
     return np.einsum("nhm,hmc->nc", w, _f64(Z)) + _f64(b3)
 
 
-def build_state(x, W, H: int, M: int, inv_tau: float, tile: int | None = None, eps: float = 0.0):
-    """Physical-state caching (section 3.3): accumulate over tiles, finalize,
-    attend, project.  Returns dict with s_raw, d, s, s1 and Z (= s'_out)."""
-    x = _f64(x)
-    N, C = x.shape
-    tile = N if not tile else tile
-    s_raw = np.zeros((H, M, C))
-    d = np.zeros((H, M))
-    for t0 in range(0, N, max(tile, 1)):
-        sr, dt = slice_accumulate(x[t0:t0 + tile], W["W2"], W["b2"], H, M, inv_tau)
-        s_raw += sr
-        d += dt
+def token_side(s_raw, d, W, H: int, eps: float = 0.0):
+    """Eq. (3) after the sums over the mesh, and section 3.3's cached state:
+    s = Linear1(d^-1 s_raw), s' = Attention(s), Z = s'_out = Linear3(s')."""
     s = slice_finalize(s_raw, d, W["W1"], W["b1"], H, eps)
     s1 = token_attention(s, W["Wq"], W["Wk"], W["Wv"])
-    Z = linear3_tokens(s1, W["W3"])
-    return {"s_raw": s_raw, "d": d, "s": s, "s1": s1, "Z": Z}
+    return {"s": s, "s1": s1, "Z": linear3_tokens(s1, W["W3"])}
+
+
+def build_state(x, W, H: int, M: int, inv_tau: float, tile: int | None = None, eps: float = 0.0):
+    """The physical state of Eq. (3): s_raw = w^T x and d = sum_i w_i over the
+    whole mesh, then the token side.  Returns s_raw, d, s, s1 and Z (= s'_out).
+
+    The two sums are additive over any partition of the mesh (Eq. (4)); a
+    `tile` only splits the mesh into consecutive parts of that many points to
+    bound the memory of w, and the parts' sums are added in order."""
+    x = _f64(x)
+    N, C = x.shape
+    parts = [x] if not tile or N <= tile else [x[i:i + tile] for i in range(0, N, tile)]
+    sums = [slice_accumulate(p, W["W2"], W["b2"], H, M, inv_tau) for p in parts]
+    s_raw = sum((t[0] for t in sums), np.zeros((H, M, C)))
+    d = sum((t[1] for t in sums), np.zeros((H, M)))
+    return {"s_raw": s_raw, "d": d, **token_side(s_raw, d, W, H, eps)}
 
 
 def layer_forward_fast(x, W, H: int, M: int, inv_tau: float, tile: int | None = None,
                        chunk: int | None = None, eps: float = 0.0) -> np.ndarray:
-    """Algorithm 1: tiled slice accumulation, token-side Linear1/attention/Linear3,
-    then chunked decoding with recomputed slice weights (Eq. (5))."""
+    """The reordered layer: the state of Eq. (3) over the whole mesh, then every
+    point decoded from it by Eq. (5).  `tile` and `chunk` only bound memory
+    (Eq. (4) and the point-wise decode make the result independent of them)."""
     x = _f64(x)
-    st = build_state(x, W, H, M, inv_tau, tile, eps)
-    N = len(x)
-    chunk = N if not chunk else chunk
-    out = np.empty((N, x.shape[1]))
-    for c0 in range(0, N, max(chunk, 1)):
-        out[c0:c0 + chunk] = deslice(x[c0:c0 + chunk], W["W2"], W["b2"], st["Z"], W["b3"],
-                                     H, M, inv_tau)
-    return out
+    Z = build_state(x, W, H, M, inv_tau, tile, eps)["Z"]
+    if not chunk or len(x) <= chunk:
+        return deslice(x, W["W2"], W["b2"], Z, W["b3"], H, M, inv_tau)
+    return np.concatenate([deslice(x[c:c + chunk], W["W2"], W["b2"], Z, W["b3"], H, M, inv_tau)
+                           for c in range(0, len(x), chunk)])

@@ -4,9 +4,9 @@ TEST INFRASTRUCTURE (see ``physics_attention.py``): only the tests, the smoke
 check and the benchmark's CPU baseline use it.  It adds no arithmetic of its
 own.  Workers run the oracle's ``slice_accumulate`` on one tile, or its
 ``deslice`` on one chunk.  The parent adds the tile terms in tile-index order
-(the sum over tiles of Eq. (4)), in the same order and from the same zero start
-as ``build_state``, so both give bitwise equal results.  It then runs the token
-side (``slice_finalize``, ``token_attention``, ``linear3_tokens``) once.
+(Eq. (4): the state's sums are additive over parts of the mesh), in the same
+order and from the same zero start as ``build_state``, so both give bitwise
+equal results.  It then runs the token side (``token_side``) once.
 
 Workers are started with "spawn" (they never inherit a GPU context) and each
 limits its BLAS to one thread, so a pool of P workers uses P cores.
@@ -84,15 +84,11 @@ class OraclePool:
     def state(self, x, W, H: int, M: int, inv_tau: float, tile: int = 65536, eps: float = 0.0):
         """The oracle's ``build_state(x, W, H, M, inv_tau, tile, eps)``, tiles in parallel."""
         C = np.asarray(x).shape[1]
-        s_raw = np.zeros((H, M, C))
-        d = np.zeros((H, M))
-        for sr, dt in self.tile_sums(x, W["W2"], W["b2"], H, M, inv_tau, tile):
-            s_raw += sr
-            d += dt
-        s = PA.slice_finalize(s_raw, d, W["W1"], W["b1"], H, eps)
-        s1 = PA.token_attention(s, W["Wq"], W["Wk"], W["Wv"])
-        Z = PA.linear3_tokens(s1, W["W3"])
-        return {"s_raw": s_raw, "d": d, "s": s, "s1": s1, "Z": Z}
+        parts = self.tile_sums(x, W["W2"], W["b2"], H, M, inv_tau, tile) if len(x) > tile else \
+            [PA.slice_accumulate(np.asarray(x, dtype=np.float64), W["W2"], W["b2"], H, M, inv_tau)]
+        s_raw = sum((t[0] for t in parts), np.zeros((H, M, C)))
+        d = sum((t[1] for t in parts), np.zeros((H, M)))
+        return {"s_raw": s_raw, "d": d, **PA.token_side(s_raw, d, W, H, eps)}
 
     def decode(self, x, W2, b2, Z, b3, H: int, M: int, inv_tau: float, chunk: int = 65536):
         """The oracle's ``deslice`` over x, chunks in parallel -> [N, C]."""
