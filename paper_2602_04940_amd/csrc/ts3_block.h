@@ -9,9 +9,9 @@
 //
 //   k_layernorm     LN1 of the first block (later blocks get theirs from the
 //                   previous block's feed-forward epilogue).
-//   k_prep_mlp      W_a and W_b as bf16 matrix-core fragments, chunked by 64
-//                   hidden units: [F/64][W_a^T part | W_b part], 64*C elements
-//                   each, so one linear copy stages a chunk.
+//   k_prep_mlp      W_a (bf16) and W_b (f16) as matrix-core fragments, chunked
+//                   by 64 hidden units: [F/64][W_a^T part | W_b part], 64*C
+//                   elements each, so one linear copy stages a chunk.
 //   k_mlp_residual  one kernel for the rest of the block: y = x + PA output,
 //                   LN2, both feed-forward products with the exact GELU between
 //                   them, the residual, and optionally the next block's LN1.
@@ -23,10 +23,11 @@
 // accumulator out^T[c][p]; the hidden layer
 // is walked in 64-unit chunks staged in LDS (two slots, one chunk ahead):
 //   GEMM1  H^T[f][p] = W_a^T[f][:] . LN2(y)[p][:] + b_a[f]   (A = staged W_a^T)
-//   GELU   in registers; the 16 x 4 outputs of two hidden tiles are exactly a
-//          B fragment of the second product (K slot (g, t) <-> hidden unit
-//          32km + 16(t>>2) + 4g + (t&3)), so h never leaves registers;
-//   GEMM2  out^T[c][p] += W_b^T[c][:] . h[p][:]                (A = staged W_b)
+//   GELU   in registers, on packed halves; the 16 x 4 outputs of two hidden
+//          tiles are exactly a B fragment of the second product (K slot
+//          (g, t) <-> hidden unit 32km + 16(t>>2) + 4g + (t&3)), so h never
+//          leaves registers;
+//   GEMM2  out^T[c][p] += W_b^T[c][:] . h[p][:]   (A = staged W_b, f16 x f16)
 // Output rows of W_b's fragments follow zchan(), so a lane ends up holding the
 // eight consecutive channels 32k + 8g .. +7 of its point: the same channels
 // it loaded, which keeps the residual and the next LayerNorm in registers.
@@ -38,17 +39,43 @@ namespace ts3 {
 
 constexpr float BLOCK_LN_EPS = 1e-5f;
 
-// erf by Abramowitz & Stegun, Handbook of Mathematical Functions, formula
-// 7.1.26 (|error| <= 1.5e-7; the hidden activations are stored as bf16).
-__device__ __forceinline__ float erf_as(float x) {
-    const float a = fabsf(x);
-    const float t = __builtin_amdgcn_rcpf(1.f + 0.3275911f * a);
-    const float poly = t * (0.254829592f + t * (-0.284496736f + t * (1.421413741f + t * (-1.453152027f +
-                                                                                           t * 1.061405429f))));
-    const float e = 1.f - poly * __builtin_amdgcn_exp2f(-a * a * 1.4426950408889634f);
-    return copysignf(e, x);
+// GELU(x) = x Phi(x) of two values, evaluated on packed halves.  Phi by
+// Abramowitz & Stegun, formula 26.2.17 (|error| < 7.5e-8 in exact
+// arithmetic): with t = 1 / (1 + 0.2316419 |x|) and
+// h = exp(-x^2 / 2) (c1 t + ... + c5 t^5), c_k = b_k / sqrt(2 pi), the lower
+// tail Phi(-|x|) is h, so Phi(x) = h for x < 0 and 1 - h for x >= 0; taking
+// the tail directly avoids the cancellation of 1 + erf at negative x.  In
+// half precision (every operation rounded to f16) the RMS relative error over
+// N(0, 1.5^2) inputs is 1.2e-3, as large as rounding the exact value to bf16
+// (the hidden activations' former storage); the worst relative error is 1e-2
+// where |GELU| is near 1e-3, and the worst absolute error 4e-3 is the f16
+// rounding of x near 8.  Pre-activations beyond the f16 range (65504) would
+// overflow; LayerNorm'd inputs through a 4C-wide layer stay orders of
+// magnitude below it.  Returns the pair as the f16 B-operand slots of the
+// second product.
+__device__ __forceinline__ f16x2 gelu2_f16(float a, float b) {
+    const f16x2 x{(_Float16)a, (_Float16)b};
+    const f16x2 ax = __builtin_elementwise_abs(x);
+    const f16x2 den = ax * (_Float16)0.2316419f + (_Float16)1.0f;
+    f16x2 t;
+    t[0] = __builtin_amdgcn_rcph(den[0]);
+    t[1] = __builtin_amdgcn_rcph(den[1]);
+    f16x2 p = t * (_Float16)0.5307027145f + (_Float16)-0.7265760136f;
+    p = p * t + (_Float16)0.7107068703f;
+    p = p * t + (_Float16)-0.1422483683f;
+    p = p * t + (_Float16)0.1274147958f;
+    p = p * t;
+    const f16x2 h = p * __builtin_elementwise_exp2(x * x * (_Float16)-0.7213475204f);  // exp(-x^2/2)
+    const f16x2 up = (_Float16)1.0f - h;
+    uint32_t m, phi;
+    // m: each half all ones where x < 0 (both halves shifted by 15: the count
+    // comes from a register, since an inline constant would reach the high
+    // half as zero); phi = x < 0 ? h : 1 - h, half by half
+    asm("v_pk_ashrrev_i16 %0, %1, %2" : "=v"(m) : "s"(0x000F000Fu), "v"(__builtin_bit_cast(uint32_t, x)));
+    asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(phi)
+        : "v"(m), "v"(__builtin_bit_cast(uint32_t, h)), "v"(__builtin_bit_cast(uint32_t, up)));
+    return x * __builtin_bit_cast(f16x2, phi);
 }
-__device__ __forceinline__ float gelu_exact(float x) { return 0.5f * x * (1.f + erf_as(x * 0.70710678118654752f)); }
 
 __device__ __forceinline__ void unpack8(const uint4 &u, float (&v)[8]) {
     const uint32_t w[4] = {u.x, u.y, u.z, u.w};
@@ -141,7 +168,8 @@ __global__ void k_prep_mlp(const float *__restrict__ Wa, const float *__restrict
             const int km = r2 % Cfg::KM, ct = r2 / Cfg::KM;
             const int64_t f = 64 * j + 32 * km + 16 * (t >> 2) + 4 * (l >> 4) + (t & 3);
             const int c = zchan(ct, l & 15);
-            v = Wb[f * C + c];
+            frag[i].bits = __builtin_bit_cast(uint16_t, (_Float16)Wb[f * C + c]);  // f16: the second product
+            continue;
         }
         frag[i].bits = __builtin_bit_cast(uint16_t, (__bf16)v);
     }
@@ -263,23 +291,26 @@ __global__ __launch_bounds__(512 / PT, 1) void k_mlp_residual(
 #pragma unroll
                 for (int pt = 0; pt < PT; ++pt) mma(Hh[ht][pt], a1[kc & 1][ht], yb[pt][kc]);
         }
-        Frag<bf16_t> a2[2][KM];
-        auto read2 = [&](int ct, Frag<bf16_t>(&dst)[KM]) {
+        Frag<f16_t> a2[2][KM];
+        auto read2 = [&](int ct, Frag<f16_t>(&dst)[KM]) {
 #pragma unroll
             for (int km = 0; km < KM; ++km)
-                dst[km].v = *reinterpret_cast<const bf16x8 *>(wb + ((ct * KM + km) * 64 + lane) * 16);
+                dst[km].v = *reinterpret_cast<const f16x8 *>(wb + ((ct * KM + km) * 64 + lane) * 16);
         };
         read2(0, a2[0]);  // in flight during the GELU
-        Frag<bf16_t> hb[PT][KM];
+        Frag<f16_t> hb[PT][KM];
 #pragma unroll
         for (int pt = 0; pt < PT; ++pt)
 #pragma unroll
-            for (int km = 0; km < KM; ++km)
+            for (int km = 0; km < KM; ++km) {
+                u32x4 u;
 #pragma unroll
                 for (int t = 0; t < 8; t += 2) {
                     const int ht = 2 * km + (t >> 2);
-                    hb[pt][km].set2(t, gelu_exact(Hh[ht][pt][t & 3]), gelu_exact(Hh[ht][pt][(t & 3) + 1]));
+                    u[t >> 1] = __builtin_bit_cast(uint32_t, gelu2_f16(Hh[ht][pt][t & 3], Hh[ht][pt][(t & 3) + 1]));
                 }
+                hb[pt][km].v = __builtin_bit_cast(f16x8, u);
+            }
 #pragma unroll
         for (int ct = 0; ct < CT; ++ct) {
             if (ct + 1 < CT) read2(ct + 1, a2[(ct + 1) & 1]);

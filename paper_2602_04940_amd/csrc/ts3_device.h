@@ -45,7 +45,22 @@ template <> struct Frag<bf16_t> {
     }
 };
 
+// IEEE half precision operands (the feed-forward's second product).  Same
+// 16-bit fragment layout as bf16.
+struct f16_t {
+    uint16_t bits;
+};
+typedef __attribute__((ext_vector_type(8))) _Float16 f16x8;
+typedef __attribute__((ext_vector_type(2))) _Float16 f16x2;
+
+template <> struct Frag<f16_t> {
+    f16x8 v;
+};
+
 // acc += A * B over one K32 step.
+__device__ __forceinline__ void mma(f32x4 &acc, const Frag<f16_t> &a, const Frag<f16_t> &b) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a.v, b.v, acc, 0, 0, 0);
+}
 __device__ __forceinline__ void mma(f32x4 &acc, const Frag<bf16_t> &a, const Frag<bf16_t> &b) {
     acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v, b.v, acc, 0, 0, 0);
 }
