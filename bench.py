@@ -132,8 +132,9 @@ def pmc_driver(points: int, workloads=("layer",)):
 # Kernels whose counters are summarised: name prefix -> (points per dispatch,
 # matrix flop per point that the kernel executes, algorithmic HBM bytes per
 # point, peak TFLOP/s of its matrix dtype).  Forward passes execute 4*C*H*M
-# (logits and one contraction); the backward's head kernels 4 and 8 and its dx
-# kernel 10 (x C*H*M), of which the backward as a whole needs 14.
+# (logits and one contraction); the backward's dZ kernel 4, its dx kernel 10
+# and its dW2 kernel 2 (x C*H*M), of which the backward as a whole needs 14.
+# The dx kernel writes dz (H*M floats per point), which the dW2 kernel reads.
 SQ_COUNTERS = ("SQ_INSTS_MFMA SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU SQ_INSTS_VALU_TRANS_F32 "
                "SQ_INSTS_LDS SQ_LDS_BANK_CONFLICT SQ_LDS_IDX_ACTIVE SQ_BUSY_CYCLES GRBM_GUI_ACTIVE")
 COUNTER_KERNELS = {
@@ -142,9 +143,9 @@ COUNTER_KERNELS = {
     "k_slice_accumulate_wide<": (1_000_000, 4 * 256 * 512, 512, PEAK_BF16_TFLOPS),
     "k_deslice_wide<": (1_000_000, 4 * 256 * 512, 1024, PEAK_BF16_TFLOPS),
     "k_mlp_residual<": (1_000_000, 4 * 256 * 1024, 1536, PEAK_BF16_TFLOPS),
-    "k_bw_head<128, 64, 0>": (1_000_000, 4 * 128 * 512, 1024, 157.3),
-    "k_bw_head<128, 64, 1>": (1_000_000, 8 * 128 * 512, 1024, 157.3),
-    "k_bw_dx<": (1_000_000, 10 * 128 * 512, 1536, 157.3),
+    "k_bw_head<": (1_000_000, 4 * 128 * 512, 1024, 157.3),
+    "k_bw_dx<": (1_000_000, 10 * 128 * 512, 1536 + 4 * 512, 157.3),
+    "k_bw_dw2<": (1_000_000, 2 * 128 * 512, 512 + 4 * 512, 157.3),
 }
 
 

@@ -204,13 +204,18 @@ ts3_status ts3_layer_forward_noalloc(const ts3_desc *desc, const ts3_weights *w,
  * Given the output gradient g = dL/dx_out [N, C], writes dx = dL/dx [N, C]
  * and the weight gradients.  The state must hold the forward of the same x
  * and weights (ts3_layer_forward, or accumulate/finalize/attention over all N
- * points): it supplies s_raw, d, s, s' and Z.  Three passes over the points,
- * in tiles of `tile` points (a multiple of group_span): dZ = sum_i w_i^T g_i;
+ * points): it supplies s_raw, d, s, s' and Z.  Passes over the points, in
+ * tiles of `tile` points (a multiple of group_span): dZ = sum_i w_i^T g_i;
  * then, after the token-side backward (Linear3, attention, Linear1, d^-1),
- * dW2 and db2; then dx.  Sums over points are folded in index order, so the
- * result does not depend on `tile`.  Float32 storage only
- * (TS3_ERR_UNSUPPORTED for bfloat16).  x, g, dx are 16-byte aligned device
- * pointers of N*C floats.  Allocates nothing; leaves the state ATTENDED. */
+ * per tile dx, which also stores the softmax gradient dz of the tile's
+ * points, and from the stored dz the tile's share of dW2 and db2.  Sums over
+ * points are folded in index order, so the result does not depend on `tile`.
+ * Float32 storage only (TS3_ERR_UNSUPPORTED for bfloat16).  x, g, dx are
+ * 16-byte aligned device pointers of N*C floats.  The dz store holds
+ * min(tile, N)*H*M floats (2 GB for 1M-point tiles at H*M = 512); the first
+ * call, or a later one with a larger tile, allocates it and the state keeps
+ * it (ts3_state_bytes counts it; TS3_ERR_OUT_OF_MEMORY if it does not fit).
+ * Leaves the state ATTENDED. */
 ts3_status ts3_layer_backward(ts3_state *st, const ts3_weights *w, const void *x, const void *g, int64_t N,
                               int64_t tile, void *dx, const ts3_grads *grads, void *stream);
 

@@ -65,11 +65,13 @@ struct Kernels {
     hipError_t (*pass2)(const void *, int64_t, int32_t, const void *, const float *, const void *, void *,
                         hipStream_t);
     // Backward (float32 storage only; NULL for bfloat16).
-    void (*bw_head)(int, const float *, const float *, int64_t, int64_t, int32_t, int32_t, int32_t,
-                    const float *, const float *, const float *, const float *, const float *, float, float *,
-                    hipStream_t);
+    void (*bw_head)(const float *, const float *, int64_t, int64_t, int32_t, int32_t, int32_t, const float *,
+                    const float *, float *, hipStream_t);
     void (*bw_dx)(const float *, const float *, int64_t, int32_t, const float *, const float *, const float *,
-                  const float *, const float *, const float *, const float *, float, float *, hipStream_t);
+                  const float *, const float *, const float *, const float *, float, float *, float *,
+                  hipStream_t);
+    void (*bw_dw2)(const float *, const float *, int64_t, int64_t, int32_t, int32_t, int32_t, float *,
+                   hipStream_t);
 };
 
 template <typename T, int C, int M>
@@ -168,15 +170,17 @@ hipError_t launch_pass2(const void *x, int64_t n, int32_t H, const void *w2p, co
 }
 
 template <int C, int M>
-void launch_bw_head(int mode, const float *x, const float *g, int64_t n, int64_t span0, int32_t Q, int32_t nspan,
-                    int32_t H, const float *w2p, const float *b2s, const float *Z, const float *dsr,
-                    const float *dd, float inv_tau, float *partials, hipStream_t st) {
-    if (mode == 0)
-        hipLaunchKernelGGL((k_bw_head<C, M, 0>), dim3((unsigned)(nspan * H)), dim3(256), 0, st, x, g, n, span0, Q,
-                           nspan, H, w2p, b2s, Z, dsr, dd, inv_tau, partials);
-    else
-        hipLaunchKernelGGL((k_bw_head<C, M, 1>), dim3((unsigned)(nspan * H)), dim3(256), 0, st, x, g, n, span0, Q,
-                           nspan, H, w2p, b2s, Z, dsr, dd, inv_tau, partials);
+void launch_bw_head(const float *x, const float *g, int64_t n, int64_t span0, int32_t Q, int32_t nspan,
+                    int32_t H, const float *w2p, const float *b2s, float *partials, hipStream_t st) {
+    hipLaunchKernelGGL((k_bw_head<C, M>), dim3((unsigned)(nspan * H)), dim3(256), 0, st, x, g, n, span0, Q, H, w2p,
+                       b2s, partials);
+}
+
+template <int C, int M>
+void launch_bw_dw2(const float *x, const float *dzs, int64_t n, int64_t span0, int32_t Q, int32_t nspan, int32_t H,
+                   float *partials, hipStream_t st) {
+    hipLaunchKernelGGL((k_bw_dw2<C, M>), dim3((unsigned)(nspan * H)), dim3(512), 0, st, x, dzs, n, span0, Q, H,
+                       partials);
 }
 
 constexpr int BW_DX_TILES_PER_WAVE = 2;  // each L2 A fragment serves two 16-point tiles
@@ -184,19 +188,20 @@ constexpr int BW_DX_TILES_PER_WAVE = 2;  // each L2 A fragment serves two 16-poi
 template <int C, int M>
 void launch_bw_dx(const float *x, const float *g, int64_t n, int32_t H, const float *w2p, const float *b2s,
                   const float *W2, const float *Z, const float *dsr, const float *dsT, const float *dd,
-                  float inv_tau, float *dx, hipStream_t st) {
+                  float inv_tau, float *dx, float *dzs, hipStream_t st) {
     constexpr int NT = BW_DX_TILES_PER_WAVE;
     hipLaunchKernelGGL((k_bw_dx<C, M, NT>), dim3((unsigned)((n + 64 * NT - 1) / (64 * NT))), dim3(256), 0, st, x, g,
-                       n, H, w2p, b2s, W2, Z, dsr, dsT, dd, inv_tau, dx);
+                       n, H, w2p, b2s, W2, Z, dsr, dsT, dd, inv_tau, dx, dzs);
 }
 
 template <typename T, int C, int M> Kernels make_kernels() {
     if constexpr (C > 128 && sizeof(T) == 4)
-        return Kernels{nullptr, nullptr, nullptr, nullptr};  // float32 rows of 1 KB: no pass-1 kernel
+        return Kernels{nullptr, nullptr, nullptr, nullptr, nullptr};  // float32 rows of 1 KB: no pass-1 kernel
     else if constexpr (sizeof(T) == 4)
-        return Kernels{&launch_pass1<T, C, M>, &launch_pass2<T, C, M>, &launch_bw_head<C, M>, &launch_bw_dx<C, M>};
+        return Kernels{&launch_pass1<T, C, M>, &launch_pass2<T, C, M>, &launch_bw_head<C, M>, &launch_bw_dx<C, M>,
+                       &launch_bw_dw2<C, M>};
     else
-        return Kernels{&launch_pass1<T, C, M>, &launch_pass2<T, C, M>, nullptr, nullptr};
+        return Kernels{&launch_pass1<T, C, M>, &launch_pass2<T, C, M>, nullptr, nullptr, nullptr};
 }
 
 bool find_kernels(int dtype, int C, int M, Kernels *k) {
@@ -229,6 +234,10 @@ struct ts3_state {
           *s1 = nullptr, *Z = nullptr, *b2s = nullptr, *b3 = nullptr;
     // backward: dZ, ds_raw [H][M][C], ds_raw transposed [H][C][M], dd [H][M], dW2^T [H][M][C]
     float *bdZ = nullptr, *bdsr = nullptr, *bdsT = nullptr, *bdd = nullptr, *bdW2T = nullptr;
+    // backward: dz [H][points][M] of one tile, allocated by the first backward
+    // whose tile needs more than it holds
+    float *bdz = nullptr;
+    int64_t bdz_points = 0;
     void *w2p = nullptr, *zp = nullptr;
     int64_t bytes = 0;
     // host bookkeeping
@@ -343,7 +352,7 @@ ts3_status ts3_state_free(ts3_state *st) {
     hipError_t e = hipDeviceSynchronize();
     void *bufs[] = {st->partials, st->runs, st->s_raw, st->dsum, st->s,    st->s1,   st->Z,
                     st->b2s,      st->b3,   st->w2p,   st->zp,   st->bdZ,  st->bdsr, st->bdsT,
-                    st->bdd,      st->bdW2T};
+                    st->bdd,      st->bdW2T, st->bdz};
     for (void *b : bufs)
         if (b) (void)hipFree(b);
     if (st->ev_fork) (void)hipEventDestroy(st->ev_fork);
@@ -678,19 +687,36 @@ ts3_status ts3_layer_backward(ts3_state *st, const ts3_weights *w, const void *x
     const int64_t HM = (int64_t)d.H * d.M;
     const float *xf = (const float *)x, *gf = (const float *)g;
     const float *w2p = (const float *)st->w2p;
-    auto head_pass = [&](int mode) -> ts3_status {
-        for (int64_t t0 = 0; t0 < N; t0 += tile) {
-            const int64_t nt = std::min(tile, N - t0);
-            st->k.bw_head(mode, xf + t0 * d.C, gf + t0 * d.C, nt, t0 / Q, (int32_t)Q, (int32_t)((nt + Q - 1) / Q),
-                          d.H, w2p, st->b2s, st->Z, st->bdsr, st->bdd, inv_tau, st->partials, hs);
-            LAUNCH_CHECK(mode == 0 ? "backward dZ pass" : "backward dW2 pass");
+    const int64_t nt_max = std::min(tile, N);
+    if (st->bdz_points < nt_max) {
+        // dz of one tile, [H][points][M]; kept by the state for later calls
+        if (st->bdz) {
+            HIP_TRY(hipStreamSynchronize(hs));
+            (void)hipFree(st->bdz);
+            st->bdz = nullptr;
+            st->bytes -= st->bdz_points * HM * 4;
+            st->bdz_points = 0;
         }
-        return TS3_OK;
-    };
+        const size_t bytes = (size_t)(nt_max * HM * 4);
+        hipError_t e = hipMalloc((void **)&st->bdz, bytes);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            st->bdz = nullptr;
+            return fail(e == hipErrorOutOfMemory ? TS3_ERR_OUT_OF_MEMORY : TS3_ERR_HIP,
+                        "hipMalloc(%zu bytes) for the backward's dz: %s", bytes, hipGetErrorString(e));
+        }
+        st->bdz_points = nt_max;
+        st->bytes += (int64_t)bytes;
+    }
     // dZ = sum_i w_i^T g_i (its column C, sum_i w_i, is not needed)
-    st->partials_fwd = false;  // the head passes reuse the span partial buffer
-    ts3_status s = head_pass(0);
-    if (s == TS3_OK) s = fold_partials(st, nspan_all, st->bdZ, st->bdd, hs);
+    st->partials_fwd = false;  // the backward passes reuse the span partial buffer
+    for (int64_t t0 = 0; t0 < N; t0 += tile) {
+        const int64_t nt = std::min(tile, N - t0);
+        st->k.bw_head(xf + t0 * d.C, gf + t0 * d.C, nt, t0 / Q, (int32_t)Q, (int32_t)((nt + Q - 1) / Q), d.H, w2p,
+                      st->b2s, st->partials, hs);
+        LAUNCH_CHECK("backward dZ pass");
+    }
+    ts3_status s = fold_partials(st, nspan_all, st->bdZ, st->bdd, hs);
     if (s != TS3_OK) return s;
     // token side: ds_raw, dd and the Linear1 / attention / Linear3 gradients
     const size_t lds = (size_t)(2 * d.M * d.C + 10 * d.M * d.dh + 2 * d.M * d.M) * 4;
@@ -700,16 +726,22 @@ ts3_status ts3_layer_backward(ts3_state *st, const ts3_weights *w, const void *x
                        w->W1, w->Wq, w->Wk, w->Wv, w->W3, d.C, d.H, d.M, d.dh, d.eps, st->bdsr, st->bdsT, st->bdd,
                        gr->dW1, gr->db1, gr->dWq, gr->dWk, gr->dWv, gr->dW3, gr->db3);
     LAUNCH_CHECK("token backward");
-    // dW2 (through its transpose per head) and db2
-    s = head_pass(1);
-    if (s == TS3_OK) s = fold_partials(st, nspan_all, st->bdW2T, gr->db2, hs);
+    // Per tile: dx (which stores dz), then the tile's span partials of dW2^T
+    // and db2 from the stored dz.
+    for (int64_t t0 = 0; t0 < N; t0 += tile) {
+        const int64_t nt = std::min(tile, N - t0);
+        st->k.bw_dx(xf + t0 * d.C, gf + t0 * d.C, nt, d.H, w2p, st->b2s, w->W2, st->Z, st->bdsr, st->bdsT, st->bdd,
+                    inv_tau, (float *)dx + t0 * d.C, st->bdz, hs);
+        LAUNCH_CHECK("backward dx pass");
+        st->k.bw_dw2(xf + t0 * d.C, st->bdz, nt, t0 / Q, (int32_t)Q, (int32_t)((nt + Q - 1) / Q), d.H,
+                     st->partials, hs);
+        LAUNCH_CHECK("backward dW2 pass");
+    }
+    s = fold_partials(st, nspan_all, st->bdW2T, gr->db2, hs);
     if (s != TS3_OK) return s;
     hipLaunchKernelGGL(k_bw_transpose_w2, dim3((unsigned)std::min<int64_t>((d.C * HM + 255) / 256, 4096)), dim3(256),
                        0, hs, st->bdW2T, d.C, (int)HM, gr->dW2);
     LAUNCH_CHECK("dW2 transpose");
-    // dx
-    st->k.bw_dx(xf, gf, N, d.H, w2p, st->b2s, w->W2, st->Z, st->bdsr, st->bdsT, st->bdd, inv_tau, (float *)dx, hs);
-    LAUNCH_CHECK("backward dx pass");
     return TS3_OK;
 }
 

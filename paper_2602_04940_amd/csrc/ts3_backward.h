@@ -4,16 +4,16 @@
 // tiling", and the Checkpoint steps of Algorithm 1).  Given the output
 // gradient g = dL/dx_out:
 //
-//   k_bw_head<MODE 0>  per (span, head): recompute w; partial dZ[m][:] =
-//                      sum_p w[p][m] g_p (and sum_p w in column C)
-//   k_bw_token         per head: back through Linear3, the attention among
-//                      the head's M tokens, Linear1 and the normalisation:
-//                      ds_raw, dd and the token-side weight gradients
-//   k_bw_head<MODE 1>  per (span, head): recompute w; dw = g.Z + x.ds_raw +
-//                      dd; dz = (1/tau) w (dw - sum_m w dw); partial
-//                      dW2^T[m][:] = sum_p dz[p][m] x_p and db2 = sum_p dz
-//   k_bw_dx            per wave block of 16-point tiles, over all heads: recompute w
-//                      and dz; dx = sum_h dz W2_h^T + w ds_raw_h
+//   k_bw_head   per (span, head): recompute w; partial dZ[m][:] =
+//               sum_p w[p][m] g_p (and sum_p w in column C)
+//   k_bw_token  per head: back through Linear3, the attention among the
+//               head's M tokens, Linear1 and the normalisation: ds_raw, dd
+//               and the token-side weight gradients
+//   k_bw_dx     per wave block of 16-point tiles, over all heads: recompute
+//               w; dw = g.Z + x.ds_raw + dd; dz = (1/tau) w (dw - sum_m w dw);
+//               dx = sum_h dz W2_h^T + w ds_raw_h; dz is stored
+//   k_bw_dw2    per (span, head): partial dW2^T[m][:] = sum_p dz[p][m] x_p
+//               and db2 = sum_p dz, from the stored dz
 //
 // Span partials are folded in index order by the forward's fold kernels, so
 // every gradient is a fixed function of the inputs (any tiling, any run).
@@ -175,19 +175,15 @@ template <int C, int M> struct BwHeadCfg {
         4 * (WAVES * WAVE_FLOATS > RED_FLOATS ? WAVES * WAVE_FLOATS : RED_FLOATS);
 };
 
-// MODE 0: partials[span][h][m][c] = sum_p w[p][m] g[p][c], column C = sum_p w.
-// MODE 1: partials[span][h][m][c] = sum_p dz[p][m] x[p][c] (dW2^T rows of head
-//         h), column C = sum_p dz (db2).
+// partials[span][h][m][c] = sum_p w[p][m] g[p][c], column C = sum_p w.
 // One workgroup per (span, head), four waves; wave v takes the span's 32-point
 // blocks v, v+4, ...; the four wave accumulators are summed in a fixed order.
 // x, gout: tile bases [n_tile][C]; the tile starts on a span boundary.
-template <int C, int M, int MODE>
+template <int C, int M>
 __global__ __launch_bounds__(256, 1) void k_bw_head(const float *__restrict__ x, const float *__restrict__ gout,
-                                                    int64_t n_tile, int64_t span0, int32_t Q, int32_t nspan,
-                                                    int32_t H, const float *__restrict__ w2p,
-                                                    const float *__restrict__ b2s, const float *__restrict__ Z,
-                                                    const float *__restrict__ dsr, const float *__restrict__ dd,
-                                                    float inv_tau, float *__restrict__ partials) {
+                                                    int64_t n_tile, int64_t span0, int32_t Q, int32_t H,
+                                                    const float *__restrict__ w2p, const float *__restrict__ b2s,
+                                                    float *__restrict__ partials) {
     using Cfg = BwHeadCfg<C, M>;
     constexpr int MT = M / 16, CT = C / 16;
     __shared__ __attribute__((aligned(16))) float lds[Cfg::LDS_BYTES / 4];
@@ -198,9 +194,8 @@ __global__ __launch_bounds__(256, 1) void k_bw_head(const float *__restrict__ x,
     const int64_t p_begin = (int64_t)span_local * Q;
     const int64_t p_end = p_begin + Q < n_tile ? p_begin + Q : n_tile;
     const int nblk = (int)((p_end - p_begin + 31) >> 5);
-    float *tt = lds + wave * Cfg::WAVE_FLOATS;  // [M][32]: w^T or dz^T
-    float *rt = tt + Cfg::TT;                   // [C][32]: g^T or x^T
-    const float *R = MODE == 0 ? gout : x;      // the contraction's point rows
+    float *tt = lds + wave * Cfg::WAVE_FLOATS;  // [M][32]: w^T
+    float *rt = tt + Cfg::TT;                   // [C][32]: g^T
 
     f32x4 S[MT][CT];
     f32x4 D[MT];
@@ -215,31 +210,21 @@ __global__ __launch_bounds__(256, 1) void k_bw_head(const float *__restrict__ x,
 
     for (int b = wave; b < nblk; b += Cfg::WAVES) {
         const int64_t p0 = p_begin + ((int64_t)b << 5);
-        // w (MODE 0) or dz (MODE 1) of the block's two 16-point tiles, as the
-        // transposed tile tt[m][p].
+        // w of the block's two 16-point tiles, as the transposed tile tt[m][p].
         {
             bool valid[2];
-            const float *xr[2], *gr[2];
+            const float *xr[2];
 #pragma unroll
             for (int pt = 0; pt < 2; ++pt) {
                 const int64_t p = p0 + 16 * pt + li;
                 valid[pt] = p < p_end;
                 const int64_t pc = valid[pt] ? p : p_end - 1;  // padding rows repeat the last point
                 xr[pt] = x + pc * C;
-                gr[pt] = gout + pc * C;
             }
             f32x4 E[2][MT];
             logits_tiles<C, M, 2>(E, w2p, b2s, h, xr, lane);
 #pragma unroll
             for (int pt = 0; pt < 2; ++pt) softmax_tile<MT>(E[pt], valid[pt]);
-            if constexpr (MODE == 1) {
-                f32x4 Dz[2][MT];
-                dz_tiles<C, M, 2>(Dz, E, Z, dsr, dd, h, xr, gr, inv_tau, lane);
-#pragma unroll
-                for (int pt = 0; pt < 2; ++pt)
-#pragma unroll
-                    for (int mt = 0; mt < MT; ++mt) E[pt][mt] = Dz[pt][mt];
-            }
 #pragma unroll
             for (int pt = 0; pt < 2; ++pt)
 #pragma unroll
@@ -252,7 +237,7 @@ __global__ __launch_bounds__(256, 1) void k_bw_head(const float *__restrict__ x,
         for (int i = lane; i < 32 * (C / 4); i += 64) {
             const int p = i / (C / 4), c4 = i % (C / 4);
             const int64_t pp = p0 + p < p_end ? p0 + p : p_end - 1;
-            const float4 v = *reinterpret_cast<const float4 *>(R + pp * C + 4 * c4);
+            const float4 v = *reinterpret_cast<const float4 *>(gout + pp * C + 4 * c4);
             rt[(4 * c4 + 0) * 32 + p] = v.x;
             rt[(4 * c4 + 1) * 32 + p] = v.y;
             rt[(4 * c4 + 2) * 32 + p] = v.z;
@@ -299,14 +284,16 @@ __global__ __launch_bounds__(256, 1) void k_bw_head(const float *__restrict__ x,
 // heads, recompute w and dz, then dx[p][c] += sum_m dz[p][m] W2[c][hM+m] +
 // w[p][m] ds_raw[h][m][c]; every A fragment (read from L2) serves the NT
 // tiles.  dsT is ds_raw transposed per head: [H][C][M].  W2 is the layer's
-// (unscaled) Linear2 weight [C][H*M].  Grid: ceil(n / (64 NT)) workgroups.
+// (unscaled) Linear2 weight [C][H*M].  dz of every point and head is also
+// written to dzs [H][n][M] (the dW2 contraction reads it there).
+// Grid: ceil(n / (64 NT)) workgroups.
 template <int C, int M, int NT>
 __global__ __launch_bounds__(256, 1) void k_bw_dx(const float *__restrict__ x, const float *__restrict__ gout,
                                                   int64_t n, int32_t H, const float *__restrict__ w2p,
                                                   const float *__restrict__ b2s, const float *__restrict__ W2,
                                                   const float *__restrict__ Z, const float *__restrict__ dsr,
                                                   const float *__restrict__ dsT, const float *__restrict__ dd,
-                                                  float inv_tau, float *__restrict__ dx) {
+                                                  float inv_tau, float *__restrict__ dx, float *__restrict__ dzs) {
     constexpr int MT = M / 16, CT = C / 16, KM = M >= 32 ? M / 32 : 1;
     const int lane = threadIdx.x & 63;
     const int wave = (int)(threadIdx.x >> 6);
@@ -336,6 +323,15 @@ __global__ __launch_bounds__(256, 1) void k_bw_dx(const float *__restrict__ x, c
 #pragma unroll
         for (int t = 0; t < NT; ++t) softmax_tile<MT>(E[t], valid[t]);
         dz_tiles<C, M, NT>(Dz, E, Z, dsr, dd, h, xr, gr, inv_tau, lane);
+        // lane (li, g) holds slices 16mt + 4g .. +3 of point p0 + 16t + li
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            if (!valid[t]) continue;
+            float *row = dzs + ((size_t)h * n + p0 + 16 * t + li) * M + 4 * g;
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+                *reinterpret_cast<float4 *>(row + 16 * mt) = float4{Dz[t][mt][0], Dz[t][mt][1], Dz[t][mt][2], Dz[t][mt][3]};
+        }
 #pragma unroll
         for (int km = 0; km < KM; ++km) {
             Frag<float> wf[NT], zf[NT];
@@ -365,6 +361,144 @@ __global__ __launch_bounds__(256, 1) void k_bw_dx(const float *__restrict__ x, c
         for (int ct = 0; ct < CT; ++ct)
             *reinterpret_cast<float4 *>(dx + p * C + ct * 16 + g * 4) =
                 float4{O[t][ct][0], O[t][ct][1], O[t][ct][2], O[t][ct][3]};
+    }
+}
+
+// dW2 span partials from the stored dz: partials[span][h][m][c] = sum_p
+// dz[h][p][m] x[p][c] over the span's points, column C = sum_p dz[h][p][m]
+// (db2).  One workgroup per (span, head), eight waves; every wave runs every
+// point of the span and owns part of the output: wave v the channel tiles ct
+// = v, v+8, ... (K = points), and wave 4 + mt the column sums of slice tile mt.
+// No wave's sum needs another's, and each is taken over the span's 64-point
+// blocks in order, so a span's partial is the same for any tiling.  Each
+// block's x and dz rows are transposed into LDS once for all eight waves
+// (two stages; the next block's rows are loaded during the current block's
+// products).  x: the tile's rows [n][C]; dzs: [H][n][M] for the same points.
+constexpr int BW_DW2_PTS = 64;  // points per block (the K of a block's products)
+constexpr int BW_DW2_LD = BW_DW2_PTS + 8;  // floats per transposed LDS row (bank spread)
+
+template <int C, int M> struct BwDw2Cfg {
+    static constexpr int XQ = C / 4, ZQ = M / 4;      // float4 per point row
+    static constexpr int XITEMS = BW_DW2_PTS * XQ;    // float4 loads per block
+    static constexpr int ZITEMS = BW_DW2_PTS * ZQ;
+    static constexpr int XPER = (XITEMS + 511) / 512;  // per thread
+    static constexpr int ZPER = (ZITEMS + 511) / 512;
+    static constexpr int STAGE = (C + M) * BW_DW2_LD;  // floats: x^T [C][LD], then dz^T [M][LD]
+};
+
+template <int C, int M>
+__global__ __launch_bounds__(512, 1) void k_bw_dw2(const float *__restrict__ x, const float *__restrict__ dzs,
+                                                   int64_t n_tile, int64_t span0, int32_t Q, int32_t H,
+                                                   float *__restrict__ partials) {
+    using Cfg = BwDw2Cfg<C, M>;
+    constexpr int MT = M / 16, CT = C / 16, NK = BW_DW2_PTS / 32, LD = BW_DW2_LD;
+    static_assert(CT <= 8 && MT <= 4, "one channel tile per wave and one column-sum tile per wave");
+    __shared__ __attribute__((aligned(16))) float lds[2 * Cfg::STAGE];
+    const int span_local = (int)blockIdx.x / H, h = (int)blockIdx.x % H;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int li = lane & 15, g = lane >> 4;
+    const int64_t p_begin = (int64_t)span_local * Q;
+    const int64_t p_end = p_begin + Q < n_tile ? p_begin + Q : n_tile;
+    const int nblk = (int)((p_end - p_begin + BW_DW2_PTS - 1) / BW_DW2_PTS);
+    const float *dzh = dzs + (size_t)h * n_tile * M;
+    const bool has_ct = wave < CT;
+    const int dmt = wave - 4;  // this wave's column-sum tile, if 0 <= dmt < MT
+    const bool has_d = dmt >= 0 && dmt < MT;
+
+    // Thread item it < ITEMS: point it % PTS, float4 column it / PTS, so a
+    // wave's transposed writes cover consecutive points of one LDS row.
+    float4 xv[Cfg::XPER], zv[Cfg::ZPER];
+    auto load = [&](int b) {
+        const int64_t pb = p_begin + (int64_t)b * BW_DW2_PTS;
+#pragma unroll
+        for (int k = 0; k < Cfg::XPER; ++k) {
+            const int it = tid + 512 * k;
+            const int p = it % BW_DW2_PTS, q = it / BW_DW2_PTS;
+            const bool ok = it < Cfg::XITEMS && pb + p < p_end;
+            xv[k] = ok ? *reinterpret_cast<const float4 *>(x + (pb + p) * C + 4 * q) : float4{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int k = 0; k < Cfg::ZPER; ++k) {
+            const int it = tid + 512 * k;
+            const int p = it % BW_DW2_PTS, q = it / BW_DW2_PTS;
+            const bool ok = it < Cfg::ZITEMS && pb + p < p_end;
+            zv[k] = ok ? *reinterpret_cast<const float4 *>(dzh + (pb + p) * M + 4 * q) : float4{0.f, 0.f, 0.f, 0.f};
+        }
+    };
+    // Rows past the span's end are zero in both operands.
+    auto store = [&](int s) {
+        float *xt = lds + s * Cfg::STAGE, *zt = xt + C * LD;
+#pragma unroll
+        for (int k = 0; k < Cfg::XPER; ++k) {
+            const int it = tid + 512 * k;
+            if (it >= Cfg::XITEMS) continue;
+            const int p = it % BW_DW2_PTS, q = it / BW_DW2_PTS;
+            xt[(4 * q + 0) * LD + p] = xv[k].x;
+            xt[(4 * q + 1) * LD + p] = xv[k].y;
+            xt[(4 * q + 2) * LD + p] = xv[k].z;
+            xt[(4 * q + 3) * LD + p] = xv[k].w;
+        }
+#pragma unroll
+        for (int k = 0; k < Cfg::ZPER; ++k) {
+            const int it = tid + 512 * k;
+            if (it >= Cfg::ZITEMS) continue;
+            const int p = it % BW_DW2_PTS, q = it / BW_DW2_PTS;
+            zt[(4 * q + 0) * LD + p] = zv[k].x;
+            zt[(4 * q + 1) * LD + p] = zv[k].y;
+            zt[(4 * q + 2) * LD + p] = zv[k].z;
+            zt[(4 * q + 3) * LD + p] = zv[k].w;
+        }
+    };
+
+    f32x4 S[MT], D = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) S[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    Frag<float> ones;
+    ones8(ones);
+
+    if (nblk > 0) {
+        load(0);
+        store(0);
+    }
+    __syncthreads();
+    for (int b = 0; b < nblk; ++b) {
+        const int s = b & 1;
+        if (b + 1 < nblk) load(b + 1);  // lands during this block's products
+        const float *xt = lds + s * Cfg::STAGE, *zt = xt + C * LD;
+#pragma unroll
+        for (int kk = 0; kk < NK; ++kk) {
+            Frag<float> a[MT];
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) frag_row(a[mt], zt + (mt * 16 + li) * LD + 32 * kk, g);
+            if (has_ct) {
+                Frag<float> bf;
+                frag_row(bf, xt + (wave * 16 + li) * LD + 32 * kk, g);
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) mma(S[mt], a[mt], bf);
+            }
+            if (has_d) {
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+                    if (mt == dmt) mma(D, a[mt], ones);
+            }
+        }
+        if (b + 1 < nblk) store(s ^ 1);  // stage s^1 was last read before the previous barrier
+        __syncthreads();
+    }
+
+    // partials[span][h][m][c]: lane (li, g) of tile (mt, ct) holds m = 16mt +
+    // 4g + r, c = 16ct + li; column-sum tiles hold the sums in every column.
+    float *dst = partials + ((size_t)(span0 + span_local) * H + h) * (size_t)(M * (C + 1));
+    if (has_ct) {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) dst[(size_t)(mt * 16 + g * 4 + r) * (C + 1) + wave * 16 + li] = S[mt][r];
+    }
+    if (has_d && li == 0) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) dst[(size_t)(dmt * 16 + g * 4 + r) * (C + 1) + C] = D[r];
     }
 }
 
