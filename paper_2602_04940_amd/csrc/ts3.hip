@@ -179,11 +179,12 @@ void launch_bw_head(const float *x, const float *g, int64_t n, int64_t span0, in
 template <int C, int M>
 void launch_bw_dw2(const float *x, const float *dzs, int64_t n, int64_t span0, int32_t Q, int32_t nspan, int32_t H,
                    float *partials, hipStream_t st) {
-    hipLaunchKernelGGL((k_bw_dw2<C, M>), dim3((unsigned)(nspan * H)), dim3(512), 0, st, x, dzs, n, span0, Q, H,
+    const int64_t places = (int64_t)BW_XCDS * ((nspan + BW_XCDS - 1) / BW_XCDS) * H;
+    hipLaunchKernelGGL((k_bw_dw2<C, M>), dim3((unsigned)places), dim3(512), 0, st, x, dzs, n, span0, Q, nspan, H,
                        partials);
 }
 
-constexpr int BW_DX_TILES_PER_WAVE = 2;  // each L2 A fragment serves two 16-point tiles
+constexpr int BW_DX_TILES_PER_WAVE = 4;  // each L2 A fragment serves four 16-point tiles
 
 template <int C, int M>
 void launch_bw_dx(const float *x, const float *g, int64_t n, int32_t H, const float *w2p, const float *b2s,

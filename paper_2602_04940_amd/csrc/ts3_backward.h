@@ -386,15 +386,23 @@ template <int C, int M> struct BwDw2Cfg {
     static constexpr int STAGE = (C + M) * BW_DW2_LD;  // floats: x^T [C][LD], then dz^T [M][LD]
 };
 
+// Grid: 8 * ceil(nspan / 8) * H workgroups.  Workgroups are dispatched to the
+// eight XCDs in turn (workgroup i to XCD i % 8); the H workgroups of a span take
+// consecutive places on one XCD, so they run together and read the span's x
+// rows through that XCD's L2 once.
+constexpr int BW_XCDS = 8;
+
 template <int C, int M>
 __global__ __launch_bounds__(512, 1) void k_bw_dw2(const float *__restrict__ x, const float *__restrict__ dzs,
-                                                   int64_t n_tile, int64_t span0, int32_t Q, int32_t H,
-                                                   float *__restrict__ partials) {
+                                                   int64_t n_tile, int64_t span0, int32_t Q, int32_t nspan,
+                                                   int32_t H, float *__restrict__ partials) {
     using Cfg = BwDw2Cfg<C, M>;
     constexpr int MT = M / 16, CT = C / 16, NK = BW_DW2_PTS / 32, LD = BW_DW2_LD;
     static_assert(CT <= 8 && MT <= 4, "one channel tile per wave and one column-sum tile per wave");
     __shared__ __attribute__((aligned(16))) float lds[2 * Cfg::STAGE];
-    const int span_local = (int)blockIdx.x / H, h = (int)blockIdx.x % H;
+    const int xcd = (int)blockIdx.x % BW_XCDS, slot = (int)blockIdx.x / BW_XCDS;
+    const int span_local = (slot / H) * BW_XCDS + xcd, h = slot % H;
+    if (span_local >= nspan) return;  // the last round's spare places (uniform, before any barrier)
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int li = lane & 15, g = lane >> 4;
