@@ -172,8 +172,9 @@ hipError_t launch_pass2(const void *x, int64_t n, int32_t H, const void *w2p, co
 template <int C, int M>
 void launch_bw_head(const float *x, const float *g, int64_t n, int64_t span0, int32_t Q, int32_t nspan,
                     int32_t H, const float *w2p, const float *b2s, float *partials, hipStream_t st) {
-    hipLaunchKernelGGL((k_bw_head<C, M>), dim3((unsigned)(nspan * H)), dim3(256), 0, st, x, g, n, span0, Q, H, w2p,
-                       b2s, partials);
+    const int64_t places = (int64_t)BW_XCDS * ((nspan + BW_XCDS - 1) / BW_XCDS) * H;
+    hipLaunchKernelGGL((k_bw_head<C, M>), dim3((unsigned)places), dim3(512), 0, st, x, g, n, span0, Q, nspan, H,
+                       w2p, b2s, partials);
 }
 
 template <int C, int M>

@@ -165,119 +165,143 @@ __device__ __forceinline__ void dz_tiles(f32x4 (&Dz)[NT][M / 16], const f32x4 (&
     }
 }
 
-template <int C, int M> struct BwHeadCfg {
-    static constexpr int WAVES = 4;
-    static constexpr int TT = M * 32;  // floats of a wave's [M][32] tile of w^T (or dz^T)
-    static constexpr int RT = C * 32;  // floats of a wave's [C][32] tile of g^T (or x^T)
-    static constexpr int WAVE_FLOATS = TT + RT;
-    static constexpr int RED_FLOATS = WAVES * M * (C + 1);
-    static constexpr int LDS_BYTES =
-        4 * (WAVES * WAVE_FLOATS > RED_FLOATS ? WAVES * WAVE_FLOATS : RED_FLOATS);
-};
+// Workgroups are dispatched to the eight XCDs in turn (workgroup i to XCD
+// i % 8).  The per-(span, head) kernels below give the H workgroups of a span
+// consecutive places on one XCD, so they run together and read the span's
+// point rows through that XCD's L2 once.  Grid: 8 * ceil(nspan / 8) * H.
+constexpr int BW_XCDS = 8;
+__device__ __forceinline__ bool bw_span_head(int nspan, int H, int &span_local, int &h) {
+    const int xcd = (int)blockIdx.x % BW_XCDS, slot = (int)blockIdx.x / BW_XCDS;
+    span_local = (slot / H) * BW_XCDS + xcd;
+    h = slot % H;
+    return span_local < nspan;
+}
 
-// partials[span][h][m][c] = sum_p w[p][m] g[p][c], column C = sum_p w.
-// One workgroup per (span, head), four waves; wave v takes the span's 32-point
-// blocks v, v+4, ...; the four wave accumulators are summed in a fixed order.
-// x, gout: tile bases [n_tile][C]; the tile starts on a span boundary.
+// dZ span partials: partials[span][h][m][c] = sum_p w[p][m] g[p][c] over the
+// span's points, column C = sum_p w[p][m].  One workgroup per (span, head),
+// eight waves, the span's points in 128-point blocks.  Wave v computes the
+// slice weights of the block's 16-point tile v (the head's W2' staged in LDS
+// once per workgroup) and writes them transposed to LDS, beside the block's
+// transposed g rows; after a barrier every wave contracts the block for its
+// own part of the output: wave v the channel tile v (K = points), waves 4 + mt
+// the column sums of slice tile mt.  No wave's sum needs another's, and each
+// runs over the blocks in order, so a span's partial is the same for any
+// tiling.  x, gout: tile bases [n_tile][C]; the tile starts on a span
+// boundary.
+constexpr int BW_HEAD_PTS = 128;             // points per block: one 16-point tile per wave
+constexpr int BW_HEAD_LD = BW_HEAD_PTS + 8;  // floats per transposed LDS row (bank spread)
+
 template <int C, int M>
-__global__ __launch_bounds__(256, 1) void k_bw_head(const float *__restrict__ x, const float *__restrict__ gout,
-                                                    int64_t n_tile, int64_t span0, int32_t Q, int32_t H,
-                                                    const float *__restrict__ w2p, const float *__restrict__ b2s,
-                                                    float *__restrict__ partials) {
-    using Cfg = BwHeadCfg<C, M>;
-    constexpr int MT = M / 16, CT = C / 16;
-    __shared__ __attribute__((aligned(16))) float lds[Cfg::LDS_BYTES / 4];
-    const int span_local = (int)blockIdx.x / H, h = (int)blockIdx.x % H;
-    const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+__global__ __launch_bounds__(512, 1) void k_bw_head(const float *__restrict__ x, const float *__restrict__ gout,
+                                                    int64_t n_tile, int64_t span0, int32_t Q, int32_t nspan,
+                                                    int32_t H, const float *__restrict__ w2p,
+                                                    const float *__restrict__ b2s, float *__restrict__ partials) {
+    constexpr int MT = M / 16, CT = C / 16, NK = BW_HEAD_PTS / 32, LD = BW_HEAD_LD;
+    constexpr int GQ = C / 4, GITEMS = BW_HEAD_PTS * GQ, GPER = GITEMS / 512;
+    static_assert(CT <= 8 && MT <= 4, "one channel tile per wave and one column-sum tile per wave");
+    static_assert(GITEMS % 512 == 0, "every thread moves the same number of g pieces");
+    __shared__ __attribute__((aligned(16))) float lds[M * C + (M + C) * LD];
+    float *const w2s = lds;         // the head's W2' fragments [MT][CK][64][8]
+    float *const wT = w2s + M * C;  // [M][LD]: w of the block, transposed
+    float *const gT = wT + M * LD;  // [C][LD]: g rows of the block, transposed
+    int span_local, h;
+    if (!bw_span_head(nspan, H, span_local, h)) return;  // uniform, before any barrier
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int li = lane & 15, g = lane >> 4;
     const int64_t p_begin = (int64_t)span_local * Q;
     const int64_t p_end = p_begin + Q < n_tile ? p_begin + Q : n_tile;
-    const int nblk = (int)((p_end - p_begin + 31) >> 5);
-    float *tt = lds + wave * Cfg::WAVE_FLOATS;  // [M][32]: w^T
-    float *rt = tt + Cfg::TT;                   // [C][32]: g^T
+    const int nblk = (int)((p_end - p_begin + BW_HEAD_PTS - 1) / BW_HEAD_PTS);
+    const bool has_ct = wave < CT;
+    const int dmt = wave - 4;  // this wave's column-sum tile, if 0 <= dmt < MT
+    const bool has_d = dmt >= 0 && dmt < MT;
 
-    f32x4 S[MT][CT];
-    f32x4 D[MT];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-        D[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int ct = 0; ct < CT; ++ct) S[mt][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+    {   // the head's W2' fragments (contiguous in w2p)
+        const float4 *src = reinterpret_cast<const float4 *>(w2p + (size_t)h * M * C);
+        for (int i = tid; i < M * C / 4; i += 512) reinterpret_cast<float4 *>(w2s)[i] = src[i];
     }
+    // g piece it: point it % PTS, float4 column it / PTS (a wave's transposed
+    // writes then cover consecutive points of one LDS row).  Rows past the
+    // span's end are zero.
+    float4 gv[GPER];
+    auto load_g = [&](int b) {
+        const int64_t pb = p_begin + (int64_t)b * BW_HEAD_PTS;
+#pragma unroll
+        for (int k = 0; k < GPER; ++k) {
+            const int it = tid + 512 * k;
+            const int p = it % BW_HEAD_PTS, q = it / BW_HEAD_PTS;
+            gv[k] = pb + p < p_end ? *reinterpret_cast<const float4 *>(gout + (pb + p) * C + 4 * q)
+                                   : float4{0.f, 0.f, 0.f, 0.f};
+        }
+    };
+    f32x4 S[MT], D = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) S[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
     Frag<float> ones;
     ones8(ones);
+    if (nblk > 0) load_g(0);
+    __syncthreads();  // W2' staged
 
-    for (int b = wave; b < nblk; b += Cfg::WAVES) {
-        const int64_t p0 = p_begin + ((int64_t)b << 5);
-        // w of the block's two 16-point tiles, as the transposed tile tt[m][p].
+    for (int b = 0; b < nblk; ++b) {
+        const int64_t pb = p_begin + (int64_t)b * BW_HEAD_PTS;
+        // w of tile `wave` (rows past the span's end repeat its last point
+        // and get zero weight)
+        f32x4 E[1][MT];
         {
-            bool valid[2];
-            const float *xr[2];
+            const int64_t p = pb + 16 * wave + li;
+            const bool valid = p < p_end;
+            const float *xr[1] = {x + (valid ? p : p_end - 1) * C};
+            logits_tiles<C, M, 1>(E, w2s, b2s + (size_t)h * M, 0, xr, lane);
+            softmax_tile<MT>(E[0], valid);
+        }
+        __syncthreads();  // every wave finished reading the previous block's tiles
 #pragma unroll
-            for (int pt = 0; pt < 2; ++pt) {
-                const int64_t p = p0 + 16 * pt + li;
-                valid[pt] = p < p_end;
-                const int64_t pc = valid[pt] ? p : p_end - 1;  // padding rows repeat the last point
-                xr[pt] = x + pc * C;
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) wT[(mt * 16 + g * 4 + r) * LD + 16 * wave + li] = E[0][mt][r];
+#pragma unroll
+        for (int k = 0; k < GPER; ++k) {
+            const int it = tid + 512 * k;
+            const int p = it % BW_HEAD_PTS, q = it / BW_HEAD_PTS;
+            gT[(4 * q + 0) * LD + p] = gv[k].x;
+            gT[(4 * q + 1) * LD + p] = gv[k].y;
+            gT[(4 * q + 2) * LD + p] = gv[k].z;
+            gT[(4 * q + 3) * LD + p] = gv[k].w;
+        }
+        if (b + 1 < nblk) load_g(b + 1);  // lands during this block's products and the next logits
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < NK; ++kk) {
+            Frag<float> a[MT];
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) frag_row(a[mt], wT + (mt * 16 + li) * LD + 32 * kk, g);
+            if (has_ct) {
+                Frag<float> bf;
+                frag_row(bf, gT + (wave * 16 + li) * LD + 32 * kk, g);
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) mma(S[mt], a[mt], bf);
             }
-            f32x4 E[2][MT];
-            logits_tiles<C, M, 2>(E, w2p, b2s, h, xr, lane);
-#pragma unroll
-            for (int pt = 0; pt < 2; ++pt) softmax_tile<MT>(E[pt], valid[pt]);
-#pragma unroll
-            for (int pt = 0; pt < 2; ++pt)
+            if (has_d) {
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) tt[(mt * 16 + g * 4 + r) * 32 + 16 * pt + li] = E[pt][mt][r];
+                    if (mt == dmt) mma(D, a[mt], ones);
+            }
         }
-        // The block's point rows, transposed: rt[c][p] (padding rows repeat the
-        // last point; their weights are zero).
-        for (int i = lane; i < 32 * (C / 4); i += 64) {
-            const int p = i / (C / 4), c4 = i % (C / 4);
-            const int64_t pp = p0 + p < p_end ? p0 + p : p_end - 1;
-            const float4 v = *reinterpret_cast<const float4 *>(gout + pp * C + 4 * c4);
-            rt[(4 * c4 + 0) * 32 + p] = v.x;
-            rt[(4 * c4 + 1) * 32 + p] = v.y;
-            rt[(4 * c4 + 2) * 32 + p] = v.z;
-            rt[(4 * c4 + 3) * 32 + p] = v.w;
-        }
-        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's tile writes landed
-        __builtin_amdgcn_wave_barrier();
-        // S[m][c] += sum_p T[p][m] R[p][c] (K = the block's 32 points).
-        Frag<float> a[MT];
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) frag_row(a[mt], tt + (mt * 16 + li) * 32, g);
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) mma(D[mt], a[mt], ones);
-#pragma unroll
-        for (int ct = 0; ct < CT; ++ct) {
-            Frag<float> bf;
-            frag_row(bf, rt + (ct * 16 + li) * 32, g);
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt) mma(S[mt][ct], a[mt], bf);
-        }
-        __builtin_amdgcn_s_waitcnt(0xc07f);  // the tiles' reads are done before the next block rewrites them
-        __builtin_amdgcn_wave_barrier();
     }
 
-    __syncthreads();
-    float *mine = lds + (size_t)wave * M * (C + 1);
+    // lane (li, g) of tile (mt, ct) holds m = 16mt + 4g + r, c = 16ct + li;
+    // column-sum tiles hold the sums in every column.
+    float *dst = partials + ((size_t)(span0 + span_local) * H + h) * (size_t)(M * (C + 1));
+    if (has_ct) {
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
+        for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int m = mt * 16 + g * 4 + r;
+            for (int r = 0; r < 4; ++r) dst[(size_t)(mt * 16 + g * 4 + r) * (C + 1) + wave * 16 + li] = S[mt][r];
+    }
+    if (has_d && li == 0) {
 #pragma unroll
-            for (int ct = 0; ct < CT; ++ct) mine[m * (C + 1) + ct * 16 + li] = S[mt][ct][r];
-            if (li == 0) mine[m * (C + 1) + C] = D[mt][r];
-        }
-    __syncthreads();
-    constexpr int E = M * (C + 1);
-    float *dst = partials + ((size_t)(span0 + span_local) * H + h) * E;
-    for (int e = threadIdx.x; e < E; e += 256)
-        dst[e] = (lds[e] + lds[E + e]) + (lds[2 * E + e] + lds[3 * E + e]);
+        for (int r = 0; r < 4; ++r) dst[(size_t)(dmt * 16 + g * 4 + r) * (C + 1) + C] = D[r];
+    }
 }
 
 // dx for wave blocks of NT 16-point tiles (four waves per workgroup): over the
@@ -374,6 +398,7 @@ __global__ __launch_bounds__(256, 1) void k_bw_dx(const float *__restrict__ x, c
 // block's x and dz rows are transposed into LDS once for all eight waves
 // (two stages; the next block's rows are loaded during the current block's
 // products).  x: the tile's rows [n][C]; dzs: [H][n][M] for the same points.
+// Grid as k_bw_head (XCD-aware).
 constexpr int BW_DW2_PTS = 64;  // points per block (the K of a block's products)
 constexpr int BW_DW2_LD = BW_DW2_PTS + 8;  // floats per transposed LDS row (bank spread)
 
@@ -386,12 +411,6 @@ template <int C, int M> struct BwDw2Cfg {
     static constexpr int STAGE = (C + M) * BW_DW2_LD;  // floats: x^T [C][LD], then dz^T [M][LD]
 };
 
-// Grid: 8 * ceil(nspan / 8) * H workgroups.  Workgroups are dispatched to the
-// eight XCDs in turn (workgroup i to XCD i % 8); the H workgroups of a span take
-// consecutive places on one XCD, so they run together and read the span's x
-// rows through that XCD's L2 once.
-constexpr int BW_XCDS = 8;
-
 template <int C, int M>
 __global__ __launch_bounds__(512, 1) void k_bw_dw2(const float *__restrict__ x, const float *__restrict__ dzs,
                                                    int64_t n_tile, int64_t span0, int32_t Q, int32_t nspan,
@@ -400,9 +419,8 @@ __global__ __launch_bounds__(512, 1) void k_bw_dw2(const float *__restrict__ x, 
     constexpr int MT = M / 16, CT = C / 16, NK = BW_DW2_PTS / 32, LD = BW_DW2_LD;
     static_assert(CT <= 8 && MT <= 4, "one channel tile per wave and one column-sum tile per wave");
     __shared__ __attribute__((aligned(16))) float lds[2 * Cfg::STAGE];
-    const int xcd = (int)blockIdx.x % BW_XCDS, slot = (int)blockIdx.x / BW_XCDS;
-    const int span_local = (slot / H) * BW_XCDS + xcd, h = slot % H;
-    if (span_local >= nspan) return;  // the last round's spare places (uniform, before any barrier)
+    int span_local, h;
+    if (!bw_span_head(nspan, H, span_local, h)) return;  // uniform, before any barrier
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int li = lane & 15, g = lane >> 4;
