@@ -16,7 +16,7 @@
 #include "../../include/ts3.h"
 #include "ts3_pass1.h"
 #include "ts3_pass1pc.h"
-#include "ts3_pass1wide.h"
+#include "ts3_pass1pcw.h"
 #include "ts3_backward.h"
 #include "ts3_pass2.h"
 #include "ts3_pass2wide.h"
@@ -78,9 +78,9 @@ template <typename T, int C, int M>
 void launch_pass1(const void *x, int64_t n, int64_t span0, int32_t Q, int32_t nspan, int32_t H,
                   const void *w2p, const float *b2s, float *partials, hipStream_t st) {
     if constexpr (sizeof(T) == 2 && C == 256) {
-        // Wide rows: channels split over the waves; XCD groups of 8 spans.
-        const int groups = (nspan + 7) / 8;
-        hipLaunchKernelGGL((k_slice_accumulate_wide<C, M>), dim3(groups * 8 * H), dim3(256), 0, st,
+        // Wide rows: two heads per workgroup, two producer and two consumer
+        // waves per head (H is even for every wide shape check_desc accepts).
+        hipLaunchKernelGGL((k_slice_accumulate_pcw<C, M>), dim3(nspan * (H / 2)), dim3(512), 0, st,
                            (const bf16_t *)x, n, span0, Q, nspan, H, (const bf16_t *)w2p, b2s, partials);
     } else if constexpr (sizeof(T) == 2 && M >= 32 && C == 128) {
         // Two heads per workgroup whenever H is even (independently of the
@@ -283,6 +283,8 @@ ts3_status check_desc(const ts3_desc *d) {
                     "M in {16,32}, C=128 with M=64, or C=256 with M=64 in bf16)", d->C, d->M);
     if ((5 * d->M * d->dh + d->M * d->M) * 4 > ATTN_LDS_MAX)
         return fail(TS3_ERR_UNSUPPORTED, "token attention needs (5*M*dh + M*M) floats <= 160 KiB of LDS");
+    if (d->C == 256 && d->H % 2 != 0)  // implied by the LDS bound at M = 64; the wide pass 1 pairs heads
+        return fail(TS3_ERR_UNSUPPORTED, "C=256 needs an even head count");
     const int64_t nspan = (d->max_points + d->group_span - 1) / d->group_span;
     if (nspan * (int64_t)d->H > (int64_t)INT32_MAX)
         return fail(TS3_ERR_UNSUPPORTED, "too many spans: raise group_span");

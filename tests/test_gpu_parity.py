@@ -128,9 +128,9 @@ def test_shapes_ragged_tiles_random_biases(C, H, M, dtype):
 
 @pytest.mark.parametrize("C,H,M", [(256, 8, 64), (256, 4, 64)])
 def test_wide_rows_bf16_ragged_spans_random_biases(C, H, M):
-    """C = 256 (the car-surface stack's width): the channel-split pass 1 with
-    128-point super-blocks; spans of 3 super-blocks, the last span and the
-    last super-block ragged."""
+    """C = 256 (the car-surface stack's width): pass 1 with two producer and
+    two consumer waves per head; spans of 12 blocks of 32 points, the last
+    span ragged."""
     N, Q, tile, chunk = 2000, 384, 768, 333
     banner(f"wide shape C={C} H={H} M={M} bf16 N={N} tile={tile} Q={Q}")
     from ts3_synth import round_bf16
