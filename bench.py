@@ -142,7 +142,7 @@ COUNTER_KERNELS = {
     "k_deslice_w8<": (1_000_000, 4 * 128 * 512, 512, PEAK_BF16_TFLOPS),
     "k_slice_accumulate_pcw<": (1_000_000, 4 * 256 * 512, 512, PEAK_BF16_TFLOPS),
     "k_deslice_wide<": (1_000_000, 4 * 256 * 512, 1024, PEAK_BF16_TFLOPS),
-    "k_mlp_residual<": (1_000_000, 4 * 256 * 1024, 1536, PEAK_BF16_TFLOPS),
+    "k_mlp_residual_pc<": (1_000_000, 4 * 256 * 1024, 1536, PEAK_BF16_TFLOPS),
     "k_bw_head<": (1_000_000, 4 * 128 * 512, 1024, 157.3),
     "k_bw_dx<": (1_000_000, 10 * 128 * 512, 1536 + 4 * 512, 157.3),
     "k_bw_dw2<": (1_000_000, 2 * 128 * 512, 512 + 4 * 512, 157.3),
@@ -579,7 +579,7 @@ def bench_stack(args):
         f"({nchunk} launches), feed-forward {t_ff:.3f} ms (1 launch + fragment prep)")
     pa_flop = 4 * wl.C * wl.H * wl.M          # per point and pass
     ff_flop = 4 * wl.C * F                    # per point: two products of 2*C*F
-    cands = [("k_mlp_residual", t_ff, 1, ff_flop * N), ("k_slice_accumulate_pcw", t_p1, ntile, pa_flop * N),
+    cands = [("k_mlp_residual_pc", t_ff, 1, ff_flop * N), ("k_slice_accumulate_pcw", t_p1, ntile, pa_flop * N),
              ("k_deslice", t_p2, nchunk, pa_flop * N)]
     kname, t_all, nl, flop_all = max(cands, key=lambda c: c[1])
     t_launch = t_all / nl

@@ -109,13 +109,14 @@ __global__ __launch_bounds__(512 / PT, 1) void k_deslice_wide(const bf16_t *__re
 #pragma unroll
                 for (int pt = 0; pt < PT; ++pt) mma(L[mt][pt], a1[kc & 1][mt], xb[pt][kc]);
         }
-        Frag<bf16_t> a2[2][KM];
-        auto read2 = [&](int ct, Frag<bf16_t>(&dst)[KM]) {
-#pragma unroll
-            for (int km = 0; km < KM; ++km)
-                dst[km].v = *reinterpret_cast<const bf16x8 *>(za + ((ct * KM + km) * 64 + lane) * 16);
-        };
-        read2(0, a2[0]);  // in flight during the softmax
+        // The decode runs with its K steps outermost: the products into one
+        // accumulator are CT * PT apart (a dependent MFMA issues at half
+        // rate); the Z fragment of step q+2 is read while step q's run.
+        constexpr int NQ = KM * CT;
+        auto zfrag = [&](int q2) { return za + (((q2 % CT) * KM + q2 / CT) * 64 + lane) * 16; };
+        Frag<bf16_t> a2[4];
+        a2[0].v = *reinterpret_cast<const bf16x8 *>(zfrag(0));  // in flight during the softmax
+        a2[1].v = *reinterpret_cast<const bf16x8 *>(zfrag(1));
         Frag<bf16_t> wb[PT][KM];
 #pragma unroll
         for (int pt = 0; pt < PT; ++pt) {
@@ -144,12 +145,11 @@ __global__ __launch_bounds__(512 / PT, 1) void k_deslice_wide(const bf16_t *__re
                 }
         }
 #pragma unroll
-        for (int ct = 0; ct < CT; ++ct) {
-            if (ct + 1 < CT) read2(ct + 1, a2[(ct + 1) & 1]);
+        for (int q2 = 0; q2 < NQ; ++q2) {
+            if (q2 + 2 < NQ) a2[(q2 + 2) & 3].v = *reinterpret_cast<const bf16x8 *>(zfrag(q2 + 2));
+            const int km = q2 / CT, ct = q2 % CT;
 #pragma unroll
-            for (int km = 0; km < KM; ++km)
-#pragma unroll
-                for (int pt = 0; pt < PT; ++pt) mma(O[ct][pt], a2[ct & 1][km], wb[pt][km]);
+            for (int pt = 0; pt < PT; ++pt) mma(O[ct][pt], a2[q2 & 3], wb[pt][km]);
         }
     }
 

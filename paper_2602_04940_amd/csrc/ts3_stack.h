@@ -18,9 +18,6 @@ struct ts3_stack {
 
 namespace {
 
-// Eight waves of 16 points (two per SIMD) measured faster than four of 32.
-constexpr int MLP_TILES_PER_WAVE = 1;
-
 struct StackKernels {
     void (*ln)(const bf16_t *, int64_t, const float *, const float *, bf16_t *, hipStream_t);
     void (*prep)(const float *, const float *, int, bf16_t *, hipStream_t);
@@ -41,9 +38,8 @@ template <int C, int F>
 void launch_mlp(const bf16_t *x, const bf16_t *pa, int64_t n, const float *l2g, const float *l2b,
                 const bf16_t *frag, const float *ba, const float *bb, const float *lng, const float *lnb, bf16_t *xo,
                 bf16_t *xn, hipStream_t st) {
-    constexpr int PT = MLP_TILES_PER_WAVE;
-    hipLaunchKernelGGL((k_mlp_residual<C, F, PT>), dim3((unsigned)((n + 127) / 128)), dim3(512 / PT), 0, st, x, pa,
-                       n, l2g, l2b, frag, ba, bb, lng, lnb, xo, xn);
+    hipLaunchKernelGGL((k_mlp_residual_pc<C, F>), dim3((unsigned)((n + 127) / 128)), dim3(512), 0, st, x, pa, n,
+                       l2g, l2b, frag, ba, bb, lng, lnb, xo, xn);
 }
 
 bool find_stack_kernels(int C, int F, StackKernels *k) {
