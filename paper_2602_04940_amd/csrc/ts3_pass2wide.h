@@ -9,8 +9,9 @@
 // already in fragment order).  Per head and wave:
 //   logits  L[m][p] = W2'_h^T x_p + b2'   (A = staged W2'^T, B = x rows kept in
 //           registers for the whole kernel)
-//   softmax max-shifted over the head's M slices (in-lane, then two
-//           cross-row swaps); the 16 x 4 outputs of two slice tiles are a B
+//   softmax over the head's M slices (in-lane, then two cross-row swaps),
+//           without the max shift while every row sum stays in the safe
+//           window (else with it); the 16 x 4 outputs of two slice tiles are a B
 //           fragment of the decode with K slot (g, t) <-> slice
 //           32km + 16(t>>2) + 4g + (t&3), the order of the prepared Z
 //   decode  out^T[c][p] += Z_h^T[c][:] . w[p][:]   (A = staged Z^T)
@@ -85,65 +86,90 @@ __global__ __launch_bounds__(512 / PT, 1) void k_deslice_wide(const bf16_t *__re
         __syncthreads();  // head h staged; every wave is done with head h-1's slot
         if (h + 1 < H) issue(h + 1, sl ^ 1);
         const unsigned char *wa = lds + sl * HB, *za = wa + PB;
-        f32x4 L[MT][PT];
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-            const float4 b = *reinterpret_cast<const float4 *>(b2s + h * M + 16 * mt + 4 * g);
-#pragma unroll
-            for (int pt = 0; pt < PT; ++pt) L[mt][pt] = f32x4{b.x, b.y, b.z, b.w};
-        }
-        // A fragments are read one K step (or channel tile) ahead of their
+        // Logits of head h.  A fragments are read one K step ahead of their
         // products, so LDS latency overlaps the matrix cores.
-        Frag<bf16_t> a1[2][MT];
-        auto read1 = [&](int kc, Frag<bf16_t>(&dst)[MT]) {
+        auto logits = [&](f32x4 (&L)[MT][PT]) {
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-                dst[mt].v = *reinterpret_cast<const bf16x8 *>(wa + ((mt * CK + kc) * 64 + lane) * 16);
+            for (int mt = 0; mt < MT; ++mt) {
+                const float4 b = *reinterpret_cast<const float4 *>(b2s + h * M + 16 * mt + 4 * g);
+#pragma unroll
+                for (int pt = 0; pt < PT; ++pt) L[mt][pt] = f32x4{b.x, b.y, b.z, b.w};
+            }
+            Frag<bf16_t> a1[2][MT];
+            auto read1 = [&](int kc, Frag<bf16_t>(&dst)[MT]) {
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+                    dst[mt].v = *reinterpret_cast<const bf16x8 *>(wa + ((mt * CK + kc) * 64 + lane) * 16);
+            };
+            read1(0, a1[0]);
+#pragma unroll
+            for (int kc = 0; kc < CK; ++kc) {
+                if (kc + 1 < CK) read1(kc + 1, a1[(kc + 1) & 1]);
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                    for (int pt = 0; pt < PT; ++pt) mma(L[mt][pt], a1[kc & 1][mt], xb[pt][kc]);
+            }
         };
-        read1(0, a1[0]);
-#pragma unroll
-        for (int kc = 0; kc < CK; ++kc) {
-            if (kc + 1 < CK) read1(kc + 1, a1[(kc + 1) & 1]);
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-                for (int pt = 0; pt < PT; ++pt) mma(L[mt][pt], a1[kc & 1][mt], xb[pt][kc]);
-        }
+        f32x4 L[MT][PT];
+        logits(L);
         // The decode runs with its K steps outermost: the products into one
         // accumulator are CT * PT apart (a dependent MFMA issues at half
         // rate); the Z fragment of step q+2 is read while step q's run.
         constexpr int NQ = KM * CT;
         auto zfrag = [&](int q2) { return za + (((q2 % CT) * KM + q2 / CT) * 64 + lane) * 16; };
-        Frag<bf16_t> a2[4];
-        a2[0].v = *reinterpret_cast<const bf16x8 *>(zfrag(0));  // in flight during the softmax
-        a2[1].v = *reinterpret_cast<const bf16x8 *>(zfrag(1));
-        Frag<bf16_t> wb[PT][KM];
+        // Softmax without the max shift while every row sum stays in the
+        // safe window; otherwise (rare) shifted, from the logits kept in L.
+        f32x4 E[MT][PT];
+        float inv[PT];
+        bool ok = true;
 #pragma unroll
         for (int pt = 0; pt < PT; ++pt) {
-            float mx = L[0][pt][0];
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) mx = fmaxf(mx, L[mt][pt][r]);
-            mx = xrow_max(mx);
             float sum = 0.f;
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    const float e = fast_exp2(L[mt][pt][r] - mx);
-                    L[mt][pt][r] = e;
-                    sum += e;
+                    E[mt][pt][r] = fast_exp2(L[mt][pt][r]);
+                    sum += E[mt][pt][r];
                 }
-            const float inv = 1.f / xrow_sum(sum);
+            sum = xrow_sum(sum);
+            ok = ok && softmax_sum_ok(sum);
+            inv[pt] = fast_rcp(sum);
+        }
+        if (__any(!ok)) {
+#pragma unroll
+            for (int pt = 0; pt < PT; ++pt) {
+                float mx = L[0][pt][0];
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) mx = fmaxf(mx, L[mt][pt][r]);
+                mx = xrow_max(mx);
+                float sum = 0.f;
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        E[mt][pt][r] = fast_exp2(L[mt][pt][r] - mx);
+                        sum += E[mt][pt][r];
+                    }
+                inv[pt] = fast_rcp(xrow_sum(sum));
+            }
+        }
+        Frag<bf16_t> wb[PT][KM];
+#pragma unroll
+        for (int pt = 0; pt < PT; ++pt)
 #pragma unroll
             for (int km = 0; km < KM; ++km)
 #pragma unroll
                 for (int t = 0; t < 8; t += 2) {
                     const int mt = 2 * km + (t >> 2);
-                    wb[pt][km].set2(t, L[mt][pt][t & 3] * inv, L[mt][pt][(t & 3) + 1] * inv);
+                    wb[pt][km].set2(t, E[mt][pt][t & 3] * inv[pt], E[mt][pt][(t & 3) + 1] * inv[pt]);
                 }
-        }
+        Frag<bf16_t> a2[4];
+        a2[0].v = *reinterpret_cast<const bf16x8 *>(zfrag(0));
+        a2[1].v = *reinterpret_cast<const bf16x8 *>(zfrag(1));
 #pragma unroll
         for (int q2 = 0; q2 < NQ; ++q2) {
             if (q2 + 2 < NQ) a2[(q2 + 2) & 3].v = *reinterpret_cast<const bf16x8 *>(zfrag(q2 + 2));

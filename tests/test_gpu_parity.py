@@ -209,12 +209,14 @@ def test_one_hot_slices_fp32():
     assert normwise(got, ref) <= FP32_TOL
 
 
-def test_bf16_shifted_softmax_fallback_mixed_with_fast_path():
-    """bf16 at the benchmark shape with a region of points whose logits overflow
-    exp2 (sums outside [2^-100, 2^100]): the blocks holding them take the
-    max-shifted path in both passes, the others the unshifted one."""
-    C, H, M, N = 128, 8, 64, 6000
-    banner("bf16 softmax fallback mixed with the fast path")
+@pytest.mark.parametrize("C,Q", [(128, 512), (256, 384)])
+def test_bf16_shifted_softmax_fallback_mixed_with_fast_path(C, Q):
+    """bf16 at the benchmark shape (and at the stack's width C = 256) with a
+    region of points whose logits overflow exp2 (sums outside [2^-100,
+    2^100]): the blocks holding them take the max-shifted path in both
+    passes, the others the unshifted one."""
+    H, M, N = 8, 64, 6000
+    banner(f"bf16 softmax fallback mixed with the fast path, C={C}")
     from ts3_synth import round_bf16
     rng = np.random.default_rng(21)
     W = make_weights(C, H, M, C // H, seed=5, bias_seed=6)
@@ -235,7 +237,7 @@ def test_bf16_shifted_softmax_fallback_mixed_with_fast_path():
     x = round_bf16(x)
     lg = (x @ W2) * it / np.log(2.0)
     assert np.abs(lg[:lo]).max() < 40 and np.abs(lg[hi:]).max() < 40   # fast-path rows elsewhere
-    got, st, _ = _run(x, W, C, H, M, "bf16", 1 / it, 1536, 1000, 512)
+    got, st, _ = _run(x, W, C, H, M, "bf16", 1 / it, 3 * Q if C == 128 else 4 * Q, 1000, Q)
     ref = oracle.layer_forward_fast(x, W, H, M, it)
     ref_st = oracle.build_state(x, W, H, M, it)
     assert_bf16_close(got, ref, "out", BF16_TOL)
