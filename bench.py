@@ -141,7 +141,7 @@ COUNTER_KERNELS = {
     "k_slice_accumulate_pc<": (1_000_000, 4 * 128 * 512, 256, PEAK_BF16_TFLOPS),
     "k_deslice_w8<": (1_000_000, 4 * 128 * 512, 512, PEAK_BF16_TFLOPS),
     "k_slice_accumulate_pcw<": (1_000_000, 4 * 256 * 512, 512, PEAK_BF16_TFLOPS),
-    "k_deslice_wide<": (1_000_000, 4 * 256 * 512, 1024, PEAK_BF16_TFLOPS),
+    "k_deslice_pc<": (1_000_000, 4 * 256 * 512, 1024, PEAK_BF16_TFLOPS),
     "k_mlp_residual_pc<": (1_000_000, 4 * 256 * 1024, 1536, PEAK_BF16_TFLOPS),
     "k_bw_head<": (1_000_000, 4 * 128 * 512, 1024, 157.3),
     "k_bw_dx<": (1_000_000, 10 * 128 * 512, 1536 + 4 * 512, 157.3),

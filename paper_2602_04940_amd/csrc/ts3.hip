@@ -17,9 +17,9 @@
 #include "ts3_pass1.h"
 #include "ts3_pass1pc.h"
 #include "ts3_pass1pcw.h"
+#include "ts3_pass2pc.h"
 #include "ts3_backward.h"
 #include "ts3_pass2.h"
-#include "ts3_pass2wide.h"
 #include "ts3_small.h"
 
 using namespace ts3;
@@ -115,8 +115,6 @@ int device_cu_count() {
     return c;
 }
 
-// Eight waves of 16 points (two per SIMD) measured faster than four of 32.
-constexpr int PASS2_WIDE_TILES_PER_WAVE = 1;
 
 template <typename T, int C, int M>
 hipError_t launch_pass2(const void *x, int64_t n, int32_t H, const void *w2p, const float *b2s,
@@ -124,10 +122,16 @@ hipError_t launch_pass2(const void *x, int64_t n, int32_t H, const void *w2p, co
     using Cfg = Pass2Cfg<T, C, M>;
     const int64_t nblk = (n + Cfg::POINTS_PER_WG - 1) / Cfg::POINTS_PER_WG;
     if constexpr (sizeof(T) == 2 && C == 256) {
-        // Wide rows: heads streamed through LDS, 128 points per workgroup.
-        constexpr int PT = PASS2_WIDE_TILES_PER_WAVE;
-        hipLaunchKernelGGL((k_deslice_wide<C, M, PT>), dim3((unsigned)((n + 127) / 128)), dim3(512 / PT), 0, st,
-                           (const bf16_t *)x, n, H, (const bf16_t *)w2p, b2s, (const bf16_t *)zp, (bf16_t *)out);
+        // Producer and consumer waves, heads streamed through LDS, persistent
+        // workgroups of 128-point blocks.  (At C = 128 the same kernel ran
+        // 22% slower than the eight-wave one below: the producer's softmax is
+        // twice as large against its MFMAs.)
+        using PCfg = Pass2PCCfg<C, M>;
+        const int64_t blocks = (n + PCfg::POINTS_PER_WG - 1) / PCfg::POINTS_PER_WG;
+        const int64_t grid = std::min<int64_t>(blocks, device_cu_count());
+        if (grid > 0)
+            hipLaunchKernelGGL((k_deslice_pc<C, M>), dim3((unsigned)grid), dim3(512), 0, st, (const bf16_t *)x, n, H,
+                               (const bf16_t *)w2p, b2s, (const bf16_t *)zp, (bf16_t *)out);
         return hipSuccess;
     } else if constexpr (sizeof(T) == 2 && C <= 128) {
         using WCfg = Pass2W8Cfg<T, C, M>;
