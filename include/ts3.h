@@ -54,17 +54,22 @@ typedef enum { TS3_ACCUM_FP32 = 0, TS3_ACCUM_FP64 = 1 } ts3_accum;
 
 /* Layer shape and numerics.
  *  C, H, M, dh : channels, heads, slices per head, head width; H*dh == C.
- *                Supported: (C, M) in {(64,16), (64,32), (128,16), (128,32),
- *                (128,64)}, and (256,64) with bf16 storage, with
- *                (5*M*dh + M*M) * 4 bytes <= 160 KiB (the token-attention
- *                working set); otherwise TS3_ERR_UNSUPPORTED.
+ *                Tuned matrix-core kernels serve (C, M) in {(64,16), (64,32),
+ *                (128,16), (128,32), (128,64)}, and (256,64) with bf16
+ *                storage and even H.  Any other C and M that are multiples
+ *                of 16 with C <= 512 and M <= 256 run on runtime-shape
+ *                vector kernels (same results up to float32 rounding order,
+ *                same tiling independence, far slower; no backward).  In
+ *                every case (5*M*dh + M*M) * 4 bytes <= 160 KiB (the
+ *                token-attention working set); otherwise TS3_ERR_UNSUPPORTED.
  *  temperature : tau > 0 of the slice softmax; +inf gives uniform weights.
  *  eps         : added to d before the division in finalize (the paper uses 0).
  *                A slice with d + eps <= 0 has a zero mean state.
  *  io_dtype    : ts3_dtype of x and out.  TS3_BF16 stores bf16 and computes
  *                the slice-weight and contraction products on bf16 matrix
  *                cores with float32 accumulation; TS3_FP32 uses float32
- *                matrix cores throughout.
+ *                matrix cores throughout.  The runtime-shape kernels read
+ *                either storage type and compute in float32 on vector units.
  *  group_span  : Q, points per accumulation span (1 <= Q <= 2^30).  Pass 1
  *                reduces each span to one partial and sums spans in index
  *                order, so results do not depend on how the mesh is tiled.
@@ -210,7 +215,8 @@ ts3_status ts3_layer_forward_noalloc(const ts3_desc *desc, const ts3_weights *w,
  * per tile dx, which also stores the softmax gradient dz of the tile's
  * points, and from the stored dz the tile's share of dW2 and db2.  Sums over
  * points are folded in index order, so the result does not depend on `tile`.
- * Float32 storage only (TS3_ERR_UNSUPPORTED for bfloat16).  x, g, dx are
+ * Float32 storage and the tuned shapes with C <= 128 only
+ * (TS3_ERR_UNSUPPORTED for bfloat16 or a runtime-shape layer).  x, g, dx are
  * 16-byte aligned device pointers of N*C floats.  The dz store holds
  * min(tile, N)*H*M floats (2 GB for 1M-point tiles at H*M = 512); the first
  * call, or a later one with a larger tile, allocates it and the state keeps

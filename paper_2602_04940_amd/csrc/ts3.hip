@@ -21,6 +21,7 @@
 #include "ts3_backward.h"
 #include "ts3_pass2.h"
 #include "ts3_small.h"
+#include "ts3_rt.h"
 
 using namespace ts3;
 
@@ -58,12 +59,14 @@ constexpr size_t PASS2_LDS_MAX = 160 * 1024;
 
 enum Phase { PH_RESET = 0, PH_ACCUM = 1, PH_FINAL = 2, PH_ATTEND = 3 };
 
-// Kernel entry points for one (dtype, C, M) instantiation.
+// Kernel entry points for one (dtype, C, M) instantiation, or the
+// runtime-shape kernels (rt) for the other multiples of 16.  The pass entry
+// points take C and M, which only the runtime-shape ones read.
 struct Kernels {
-    void (*pass1)(const void *, int64_t, int64_t, int32_t, int32_t, int32_t, const void *, const float *,
-                  float *, hipStream_t);
-    hipError_t (*pass2)(const void *, int64_t, int32_t, const void *, const float *, const void *, void *,
-                        hipStream_t);
+    void (*pass1)(const void *, int64_t, int64_t, int32_t, int32_t, int32_t, int32_t, int32_t, const void *,
+                  const float *, float *, hipStream_t);
+    hipError_t (*pass2)(const void *, int64_t, int32_t, int32_t, int32_t, const void *, const float *, const void *,
+                        void *, hipStream_t);
     // Backward (float32 storage only; NULL for bfloat16).
     void (*bw_head)(const float *, const float *, int64_t, int64_t, int32_t, int32_t, int32_t, const float *,
                     const float *, float *, hipStream_t);
@@ -72,10 +75,11 @@ struct Kernels {
                   hipStream_t);
     void (*bw_dw2)(const float *, const float *, int64_t, int64_t, int32_t, int32_t, int32_t, float *,
                    hipStream_t);
+    bool rt = false;  // operands in the runtime-shape layouts (k_prep_w2_rt, k_prep_z_rt)
 };
 
 template <typename T, int C, int M>
-void launch_pass1(const void *x, int64_t n, int64_t span0, int32_t Q, int32_t nspan, int32_t H,
+void launch_pass1(const void *x, int64_t n, int64_t span0, int32_t Q, int32_t nspan, int32_t H, int32_t, int32_t,
                   const void *w2p, const float *b2s, float *partials, hipStream_t st) {
     if constexpr (sizeof(T) == 2 && C == 256) {
         // Wide rows: two heads per workgroup, two producer and two consumer
@@ -117,7 +121,7 @@ int device_cu_count() {
 
 
 template <typename T, int C, int M>
-hipError_t launch_pass2(const void *x, int64_t n, int32_t H, const void *w2p, const float *b2s,
+hipError_t launch_pass2(const void *x, int64_t n, int32_t H, int32_t, int32_t, const void *w2p, const float *b2s,
                         const void *zp, void *out, hipStream_t st) {
     using Cfg = Pass2Cfg<T, C, M>;
     const int64_t nblk = (n + Cfg::POINTS_PER_WG - 1) / Cfg::POINTS_PER_WG;
@@ -210,6 +214,36 @@ template <typename T, int C, int M> Kernels make_kernels() {
         return Kernels{&launch_pass1<T, C, M>, &launch_pass2<T, C, M>, nullptr, nullptr, nullptr};
 }
 
+// Launches of at most RT_MAX_WGS workgroups (larger calls are split into
+// span or point ranges, which changes no result).
+constexpr int64_t RT_MAX_WGS = 1 << 22;
+
+template <typename T>
+void launch_pass1_rt(const void *x, int64_t n, int64_t span0, int32_t Q, int32_t nspan, int32_t H, int32_t C,
+                     int32_t M, const void *w2r, const float *b2s, float *partials, hipStream_t st) {
+    const size_t lds = (size_t)RT_PTS * (C + M) * 4;
+    const int64_t per_span = (int64_t)H * ((C + 63) / 64);
+    const int64_t batch = std::max<int64_t>(1, RT_MAX_WGS / per_span);
+    for (int64_t s0 = 0; s0 < nspan; s0 += batch) {
+        const int64_t ns = std::min<int64_t>(batch, nspan - s0);
+        hipLaunchKernelGGL(k_slice_accumulate_rt<T>, dim3((unsigned)(ns * per_span)), dim3(256), lds, st,
+                           (const T *)x + s0 * Q * C, n - s0 * Q, span0 + s0, Q, H, C, M, (const T *)w2r, b2s,
+                           partials);
+    }
+}
+template <typename T>
+hipError_t launch_pass2_rt(const void *x, int64_t n, int32_t H, int32_t C, int32_t M, const void *w2r,
+                           const float *b2s, const void *zr, void *out, hipStream_t st) {
+    const size_t lds = (size_t)RT_PTS * (C + M) * 4;
+    for (int64_t p0 = 0; p0 < n; p0 += RT_MAX_WGS * RT_PTS) {
+        const int64_t np = std::min<int64_t>(RT_MAX_WGS * RT_PTS, n - p0);
+        hipLaunchKernelGGL(k_deslice_rt<T>, dim3((unsigned)((np + RT_PTS - 1) / RT_PTS)), dim3(256), lds, st,
+                           (const T *)x + p0 * C, np, H, C, M, (const T *)w2r, b2s, (const T *)zr,
+                           (T *)out + p0 * C);
+    }
+    return hipSuccess;
+}
+
 bool find_kernels(int dtype, int C, int M, Kernels *k) {
 #define TS3_SHAPE(CC, MM)                                                                      \
     if (C == CC && M == MM) {                                                                  \
@@ -224,6 +258,25 @@ bool find_kernels(int dtype, int C, int M, Kernels *k) {
     TS3_SHAPE(256, 64)
 #undef TS3_SHAPE
     return false;
+}
+
+// The tuned kernels for (dtype, C, M), else the runtime-shape ones when C and
+// M are multiples of 16 within their limits.
+bool find_any_kernels(int dtype, int C, int M, Kernels *k) {
+    if (find_kernels(dtype, C, M, k)) return true;
+    if (C % 16 != 0 || M % 16 != 0 || C > RT_MAX_C || M > RT_MAX_M) return false;
+    *k = dtype == TS3_BF16 ? Kernels{&launch_pass1_rt<bf16_t>, &launch_pass2_rt<bf16_t>, nullptr, nullptr, nullptr}
+                           : Kernels{&launch_pass1_rt<float>, &launch_pass2_rt<float>, nullptr, nullptr, nullptr};
+    k->rt = true;
+    return true;
+}
+
+// Elements of the prepared W2' and Z buffers (fragment order, or rows for
+// the runtime-shape kernels).
+int64_t w2p_elems(const ts3_desc &d) { return (int64_t)d.H * d.M * d.C; }
+int64_t zp_elems(const ts3_desc &d, bool rt) {
+    const int KM = d.M >= 32 ? d.M / 32 : 1;
+    return rt ? (int64_t)d.H * d.M * d.C : (int64_t)d.H * (d.C / 16) * KM * 512;
 }
 
 }  // namespace
@@ -282,9 +335,9 @@ ts3_status check_desc(const ts3_desc *d) {
     if (d->max_points < 0) return fail(TS3_ERR_INVALID_ARG, "max_points must be >= 0");
     if (d->H > 4096 || d->dh > 256) return fail(TS3_ERR_UNSUPPORTED, "H <= 4096 and dh <= 256 required");
     Kernels k;
-    if (!find_kernels(d->io_dtype, d->C, d->M, &k))
-        return fail(TS3_ERR_UNSUPPORTED, "no kernel for C=%d, M=%d (supported: C in {64,128} with "
-                    "M in {16,32}, C=128 with M=64, or C=256 with M=64 in bf16)", d->C, d->M);
+    if (!find_any_kernels(d->io_dtype, d->C, d->M, &k))
+        return fail(TS3_ERR_UNSUPPORTED, "no kernel for C=%d, M=%d (C and M must be multiples of 16 with "
+                    "C <= %d and M <= %d)", d->C, d->M, RT_MAX_C, RT_MAX_M);
     if ((5 * d->M * d->dh + d->M * d->M) * 4 > ATTN_LDS_MAX)
         return fail(TS3_ERR_UNSUPPORTED, "token attention needs (5*M*dh + M*M) floats <= 160 KiB of LDS");
     if (d->C == 256 && d->H % 2 != 0)  // implied by the LDS bound at M = 64; the wide pass 1 pairs heads
@@ -304,10 +357,16 @@ ts3_status check_weights_w2(const ts3_weights *w) {
 ts3_status prep_w2(ts3_state *st, const ts3_weights *w, hipStream_t stream) {
     const ts3_desc &d = st->desc;
     const float scale = (float)(1.4426950408889634 / (double)d.temperature);
-    const int64_t total = (int64_t)d.H * (d.M / 16) * (d.C / 32) * 512;
+    const int64_t total = w2p_elems(d);
     const int grid = (int)std::min<int64_t>((total + 255) / 256, 4096);
     const int grid2 = std::max(grid, (d.H * d.M + 255) / 256);
-    if (d.io_dtype == TS3_BF16)
+    if (st->k.rt && d.io_dtype == TS3_BF16)
+        hipLaunchKernelGGL(k_prep_w2_rt<bf16_t>, dim3(grid2), dim3(256), 0, stream, w->W2, w->b2, scale, d.C, d.H,
+                           d.M, (bf16_t *)st->w2p, st->b2s);
+    else if (st->k.rt)
+        hipLaunchKernelGGL(k_prep_w2_rt<float>, dim3(grid2), dim3(256), 0, stream, w->W2, w->b2, scale, d.C, d.H,
+                           d.M, (float *)st->w2p, st->b2s);
+    else if (d.io_dtype == TS3_BF16)
         hipLaunchKernelGGL(k_prep_w2<bf16_t>, dim3(grid2), dim3(256), 0, stream, w->W2, w->b2, scale, d.C,
                            d.H, d.M, (bf16_t *)st->w2p, st->b2s);
     else
@@ -322,10 +381,15 @@ ts3_status prep_w2(ts3_state *st, const ts3_weights *w, hipStream_t stream) {
 
 ts3_status prep_z(ts3_state *st, hipStream_t stream) {
     const ts3_desc &d = st->desc;
-    const int KM = d.M >= 32 ? d.M / 32 : 1;
-    const int64_t total = (int64_t)d.H * (d.C / 16) * KM * 512;
+    const int64_t total = zp_elems(d, st->k.rt);
     const int grid = (int)std::min<int64_t>((total + 255) / 256, 4096);
-    if (d.io_dtype == TS3_BF16)
+    if (st->k.rt && d.io_dtype == TS3_BF16)
+        hipLaunchKernelGGL(k_prep_z_rt<bf16_t>, dim3(grid), dim3(256), 0, stream, st->Z, st->b3, d.C, d.H, d.M,
+                           (bf16_t *)st->zp);
+    else if (st->k.rt)
+        hipLaunchKernelGGL(k_prep_z_rt<float>, dim3(grid), dim3(256), 0, stream, st->Z, st->b3, d.C, d.H, d.M,
+                           (float *)st->zp);
+    else if (d.io_dtype == TS3_BF16)
         hipLaunchKernelGGL(k_prep_z<bf16_t>, dim3(grid), dim3(256), 0, stream, st->Z, st->b3, d.C, d.H, d.M,
                            (bf16_t *)st->zp);
     else
@@ -390,14 +454,13 @@ ts3_status ts3_state_create(const ts3_desc *desc, ts3_state **out) {
     ts3_state *st = new (std::nothrow) ts3_state();
     if (!st) return fail(TS3_ERR_OUT_OF_MEMORY, "host allocation failed");
     st->desc = *desc;
-    find_kernels(desc->io_dtype, desc->C, desc->M, &st->k);
+    find_any_kernels(desc->io_dtype, desc->C, desc->M, &st->k);
     const ts3_desc &d = st->desc;
     st->esize = d.io_dtype == TS3_BF16 ? 2 : 4;
     st->nspan_max = std::max<int64_t>(1, (d.max_points + d.group_span - 1) / d.group_span);
     st->E = (int64_t)d.H * d.M * (d.C + 1);
     st->nrun_max = (st->nspan_max + FOLD - 1) / FOLD;
     const int64_t HM = (int64_t)d.H * d.M;
-    const int KM = d.M >= 32 ? d.M / 32 : 1;
     struct Req {
         void **p;
         int64_t bytes;
@@ -411,8 +474,8 @@ ts3_status ts3_state_create(const ts3_desc *desc, ts3_state **out) {
         {(void **)&st->Z, HM * d.C * 4},
         {(void **)&st->b2s, HM * 4},
         {(void **)&st->b3, (int64_t)d.C * 4},
-        {&st->w2p, (int64_t)d.H * (d.M / 16) * (d.C / 32) * 512 * st->esize},
-        {&st->zp, (int64_t)d.H * (d.C / 16) * KM * 512 * st->esize},
+        {&st->w2p, w2p_elems(d) * st->esize},
+        {&st->zp, zp_elems(d, st->k.rt) * st->esize},
         {(void **)&st->bdZ, HM * d.C * 4},
         {(void **)&st->bdsr, HM * d.C * 4},
         {(void **)&st->bdsT, HM * d.C * 4},
@@ -495,7 +558,8 @@ ts3_status ts3_slice_accumulate(ts3_state *st, const ts3_weights *w, const void 
         s = prep_w2(st, w, hs);
         if (s != TS3_OK) return s;
     }
-    st->k.pass1(x_tile, n_tile, span0, (int32_t)Q, (int32_t)nspan, d.H, st->w2p, st->b2s, st->partials, hs);
+    st->k.pass1(x_tile, n_tile, span0, (int32_t)Q, (int32_t)nspan, d.H, d.C, d.M, st->w2p, st->b2s, st->partials,
+                hs);
     LAUNCH_CHECK("slice_accumulate");
     for (int64_t i = span0; i < span0 + nspan; ++i) st->span_written[(size_t)i] = 1;
     if (ragged) st->span_written[(size_t)(span0 + nspan - 1)] = 2;
@@ -555,8 +619,7 @@ ts3_status ts3_slice_finalize(ts3_state *st, const ts3_weights *w, void *stream)
     }
     const ts3_status s = fold_partials(st, nspan, st->s_raw, st->dsum, hs);
     if (s != TS3_OK) return s;
-    const size_t lds = (size_t)d.M * d.C * 4;
-    hipLaunchKernelGGL(k_finalize, dim3(d.H), dim3(256), lds, hs, st->s_raw, st->dsum, w->W1, w->b1, d.C, d.H,
+    hipLaunchKernelGGL(k_finalize, dim3(d.H), dim3(256), 0, hs, st->s_raw, st->dsum, w->W1, w->b1, d.C, d.H,
                        d.M, d.dh, d.eps, st->s);
     LAUNCH_CHECK("finalize");
     st->phase = PH_FINAL;
@@ -603,7 +666,7 @@ ts3_status ts3_deslice(const ts3_state *st, const ts3_weights *w, const void *x_
     const ts3_desc &d = st->desc;
     if (n_chunk > ((int64_t)INT32_MAX) * 64) return fail(TS3_ERR_INVALID_ARG, "n_chunk too large for one launch");
     const hipError_t le =
-        st->k.pass2(x_chunk, n_chunk, d.H, st->w2p, st->b2s, st->zp, out_chunk, (hipStream_t)stream);
+        st->k.pass2(x_chunk, n_chunk, d.H, d.C, d.M, st->w2p, st->b2s, st->zp, out_chunk, (hipStream_t)stream);
     if (le != hipSuccess) return fail(TS3_ERR_HIP, "deslice LDS setup: %s", hipGetErrorString(le));
     LAUNCH_CHECK("deslice");
     return TS3_OK;
@@ -675,7 +738,8 @@ ts3_status ts3_layer_backward(ts3_state *st, const ts3_weights *w, const void *x
         return fail(TS3_ERR_INVALID_ARG, "grads or one of its pointers is NULL");
     const ts3_desc &d = st->desc;
     if (d.io_dtype != TS3_FP32 || !st->k.bw_head || !st->k.bw_dx)
-        return fail(TS3_ERR_UNSUPPORTED, "the backward is built for float32 storage");
+        return fail(TS3_ERR_UNSUPPORTED, "the backward is built for float32 storage with C in {64, 128} and "
+                    "M in {16, 32, 64}");
     if (N <= 0 || tile <= 0) return fail(TS3_ERR_INVALID_ARG, "N > 0 and tile > 0 required");
     if (tile % d.group_span != 0)
         return fail(TS3_ERR_INVALID_ARG, "tile %lld is not a multiple of group_span %lld", (long long)tile,
@@ -867,7 +931,6 @@ ScratchLayout scratch_layout(const ts3_desc &d, int64_t N, int64_t tile) {
     // An empty mesh still folds one (zero) span.
     const int64_t nrun = (std::max<int64_t>((N + Q - 1) / Q, 1) + FOLD - 1) / FOLD;
     const int esize = d.io_dtype == TS3_BF16 ? 2 : 4;
-    const int KM = d.M >= 32 ? d.M / 32 : 1;
     ScratchLayout L{};
     size_t at = 0;
     auto take = [&](size_t &field, size_t bytes) { field = at; at += up(bytes); };
@@ -880,8 +943,10 @@ ScratchLayout scratch_layout(const ts3_desc &d, int64_t N, int64_t tile) {
     take(L.Z, (size_t)(HM * d.C) * 4);
     take(L.b2s, (size_t)HM * 4);
     take(L.b3, (size_t)d.C * 4);
-    take(L.w2p, (size_t)d.H * (d.M / 16) * (d.C / 32) * 512 * esize);
-    take(L.zp, (size_t)d.H * (d.C / 16) * KM * 512 * esize);
+    Kernels k;
+    find_any_kernels(d.io_dtype, d.C, d.M, &k);
+    take(L.w2p, (size_t)w2p_elems(d) * esize);
+    take(L.zp, (size_t)zp_elems(d, k.rt) * esize);
     L.total = at;
     return L;
 }
@@ -930,7 +995,7 @@ ts3_status ts3_layer_forward_noalloc(const ts3_desc *desc, const ts3_weights *w,
     // it owns nothing and is never freed.
     ts3_state st;
     st.desc = d;
-    find_kernels(d.io_dtype, d.C, d.M, &st.k);
+    find_any_kernels(d.io_dtype, d.C, d.M, &st.k);
     st.esize = d.io_dtype == TS3_BF16 ? 2 : 4;
     st.E = (int64_t)d.H * d.M * (d.C + 1);
     st.partials = (float *)(b + lay.partials);
@@ -963,8 +1028,8 @@ ts3_status ts3_layer_forward_noalloc(const ts3_desc *desc, const ts3_weights *w,
     for (int64_t t0 = 0; t0 < N; t0 += tile) {
         const int64_t nt = std::min(tile, N - t0);
         const int64_t ns = (nt + Q - 1) / Q;
-        st.k.pass1((const char *)x + t0 * d.C * st.esize, nt, 0, (int32_t)Q, (int32_t)ns, d.H, st.w2p, st.b2s,
-                   st.partials, hs);
+        st.k.pass1((const char *)x + t0 * d.C * st.esize, nt, 0, (int32_t)Q, (int32_t)ns, d.H, d.C, d.M, st.w2p,
+                   st.b2s, st.partials, hs);
         LAUNCH_CHECK("slice_accumulate");
         if (d.accum == TS3_ACCUM_FP64) fold_tile<double>(st.partials, E, t0 / Q, ns, st.runs, hs);
         else fold_tile<float>(st.partials, E, t0 / Q, ns, st.runs, hs);
@@ -978,7 +1043,7 @@ ts3_status ts3_layer_forward_noalloc(const ts3_desc *desc, const ts3_weights *w,
         hipLaunchKernelGGL(k_fold_final<float>, dim3(gx), dim3(256), 0, hs, (const float *)st.runs, E, nrun, d.C,
                            st.s_raw, st.dsum);
     LAUNCH_CHECK("fold_final");
-    hipLaunchKernelGGL(k_finalize, dim3(d.H), dim3(256), (size_t)d.M * d.C * 4, hs, st.s_raw, st.dsum, w->W1,
+    hipLaunchKernelGGL(k_finalize, dim3(d.H), dim3(256), 0, hs, st.s_raw, st.dsum, w->W1,
                        w->b1, d.C, d.H, d.M, d.dh, d.eps, st.s);
     LAUNCH_CHECK("finalize");
     st.phase = PH_FINAL;

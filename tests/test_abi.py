@@ -46,9 +46,11 @@ def _desc(**kw):
 @pytest.mark.parametrize("kw,status", [
     (dict(C=0), L.TS3_ERR_INVALID_ARG),
     (dict(H=4), L.TS3_ERR_UNSUPPORTED),           # H*dh != C
-    (dict(C=96, H=6), L.TS3_ERR_UNSUPPORTED),     # no kernel for C=96
-    (dict(M=48), L.TS3_ERR_UNSUPPORTED),
-    (dict(C=256, H=8, dh=32, io_dtype=L.TS3_FP32), L.TS3_ERR_UNSUPPORTED),  # wide rows are bf16 only
+    (dict(C=72, H=8, dh=9), L.TS3_ERR_UNSUPPORTED),         # C not a multiple of 16
+    (dict(M=24), L.TS3_ERR_UNSUPPORTED),                    # M not a multiple of 16
+    (dict(C=640, H=8, dh=80, M=16), L.TS3_ERR_UNSUPPORTED),  # C beyond the runtime-shape kernels' 512
+    (dict(M=272, H=16, dh=8), L.TS3_ERR_UNSUPPORTED),       # M beyond the runtime-shape kernels' 256
+    (dict(C=128, H=2, dh=64, M=128), L.TS3_ERR_UNSUPPORTED),  # token attention over 160 KiB of LDS
     (dict(io_dtype=7), L.TS3_ERR_INVALID_ARG),
     (dict(accum=2), L.TS3_ERR_INVALID_ARG),
     (dict(accum=-1), L.TS3_ERR_INVALID_ARG),
@@ -86,7 +88,7 @@ def test_block_weight_layout_matches_header():
     (dict(), 0, 512, L.TS3_ERR_INVALID_ARG),                                 # no blocks
     (dict(), 2, 384, L.TS3_ERR_UNSUPPORTED),                                 # hidden != 4C
     (dict(io_dtype=L.TS3_FP32), 2, 512, L.TS3_ERR_UNSUPPORTED),              # activations are bf16
-    (dict(C=256, H=8, dh=32, M=32), 2, 1024, L.TS3_ERR_UNSUPPORTED),         # no C=256, M=32 layer kernel
+    (dict(C=256, H=8, dh=32, M=24), 2, 1024, L.TS3_ERR_UNSUPPORTED),         # M not a multiple of 16
     (dict(temperature=-1.0), 2, 512, L.TS3_ERR_INVALID_ARG),
 ])
 def test_bad_stack_is_rejected_before_any_device_call(kw, blocks, hidden, status):

@@ -148,6 +148,41 @@ def test_wide_rows_bf16_ragged_spans_random_biases(C, H, M):
         assert np.array_equal(st1[k], st[k]), k
 
 
+RT_SHAPES = [(192, 4, 48, "fp32"), (192, 4, 48, "bf16"), (256, 8, 64, "fp32"), (128, 8, 128, "bf16"),
+             (96, 6, 16, "fp32"), (512, 8, 16, "bf16"), (48, 1, 80, "fp32")]
+
+
+@pytest.mark.parametrize("C,H,M,dtype", RT_SHAPES)
+def test_runtime_shape_kernels_ragged_tiles(C, H, M, dtype):
+    """Shapes without a tuned kernel (any C, M that are multiples of 16):
+    the runtime-shape vector kernels, ragged spans and chunks, tiled and
+    untiled runs bitwise equal."""
+    N, Q, tile, chunk = 1000, 160, 480, 333
+    banner(f"runtime shape C={C} H={H} M={M} {dtype} N={N} tile={tile} Q={Q}")
+    rng = np.random.default_rng(C * 1000 + H * 10 + M + 7)
+    x = rng.standard_normal((N, C))
+    if dtype == "bf16":
+        from ts3_synth import round_bf16
+        x = round_bf16(x)
+    else:
+        x = x.astype(np.float32).astype(np.float64)
+    W = make_weights(C, H, M, C // H, seed=5, bias_seed=6)
+    got, st, _ = _run(x, W, C, H, M, dtype, 0.5, tile, chunk, Q)
+    ref = oracle.layer_forward_fast(x, W, H, M, 2.0)
+    ref_st = oracle.build_state(x, W, H, M, 2.0)
+    if dtype == "fp32":
+        assert normwise(got, ref) <= FP32_TOL
+        for k in ("s_raw", "d", "Z"):
+            assert normwise(st[k], ref_st[k]) <= FP32_TOL, k
+    else:
+        assert_bf16_close(got, ref, "out", BF16_TOL)
+        assert_state_close(st, ref_st, "state", BF16_TOL)
+    got1, st1, _ = _run(x, W, C, H, M, dtype, 0.5, 1120, N, Q)
+    assert np.array_equal(got1, got)
+    for k in ("s_raw", "d", "Z"):
+        assert np.array_equal(st1[k], st[k]), k
+
+
 @pytest.mark.parametrize("Q", [96, 100])
 def test_bf16_two_head_workgroups_odd_block_counts(Q):
     """Pass 1 with two heads per workgroup: a span of Q = 96 points has three
