@@ -22,6 +22,7 @@
 #include "ts3_pass2.h"
 #include "ts3_small.h"
 #include "ts3_rt.h"
+#include "ts3_pass2sf.h"
 
 using namespace ts3;
 
@@ -75,6 +76,10 @@ struct Kernels {
                   hipStream_t);
     void (*bw_dw2)(const float *, const float *, int64_t, int64_t, int32_t, int32_t, int32_t, float *,
                    hipStream_t);
+    // Pass 2 in the slice-state form (bfloat16, head width 16): x, n, W2', b2',
+    // s'^T fragments, W3^T fragments, b3, out.  NULL where it does not apply.
+    hipError_t (*pass2sf)(const void *, int64_t, const void *, const float *, const void *, const void *,
+                          const float *, void *, hipStream_t) = nullptr;
     bool rt = false;  // operands in the runtime-shape layouts (k_prep_w2_rt, k_prep_z_rt)
 };
 
@@ -204,12 +209,35 @@ void launch_bw_dx(const float *x, const float *g, int64_t n, int32_t H, const fl
                        n, H, w2p, b2s, W2, Z, dsr, dsT, dd, inv_tau, dx, dzs);
 }
 
+template <int C, int M>
+hipError_t launch_pass2sf(const void *x, int64_t n, const void *w2p, const float *b2s, const void *sf,
+                          const void *w3f, const float *b3, void *out, hipStream_t st) {
+    using Cfg = Pass2SFCfg<C, M>;
+    // At most P2_MAX_ITERS blocks per workgroup and launch (the kernel records
+    // fallback blocks in a 64-bit mask); larger calls are split, which changes
+    // no result: every point is decoded alone.
+    const int64_t cus = device_cu_count();
+    const int64_t span = cus * P2_MAX_ITERS * Cfg::POINTS_PER_WG;
+    for (int64_t off = 0; off < n; off += span) {
+        const int64_t m = std::min<int64_t>(span, n - off);
+        const int64_t blocks = (m + Cfg::POINTS_PER_WG - 1) / Cfg::POINTS_PER_WG;
+        const int64_t grid = std::min<int64_t>(blocks, cus);
+        hipLaunchKernelGGL((k_deslice_sf<C, M>), dim3((unsigned)grid), dim3(512), 0, st,
+                           (const bf16_t *)x + off * C, m, (const bf16_t *)w2p, b2s, (const bf16_t *)sf,
+                           (const bf16_t *)w3f, b3, (bf16_t *)out + off * C);
+    }
+    return hipSuccess;
+}
+
 template <typename T, int C, int M> Kernels make_kernels() {
     if constexpr (C > 128 && sizeof(T) == 4)
         return Kernels{nullptr, nullptr, nullptr, nullptr, nullptr};  // float32 rows of 1 KB: no pass-1 kernel
     else if constexpr (sizeof(T) == 4)
         return Kernels{&launch_pass1<T, C, M>, &launch_pass2<T, C, M>, &launch_bw_head<C, M>, &launch_bw_dx<C, M>,
                        &launch_bw_dw2<C, M>};
+    else if constexpr (C <= 128 && M % 32 == 0)
+        return Kernels{&launch_pass1<T, C, M>, &launch_pass2<T, C, M>, nullptr, nullptr, nullptr,
+                       &launch_pass2sf<C, M>};
     else
         return Kernels{&launch_pass1<T, C, M>, &launch_pass2<T, C, M>, nullptr, nullptr, nullptr};
 }
@@ -298,6 +326,10 @@ struct ts3_state {
     float *bdz = nullptr;
     int64_t bdz_points = 0;
     void *w2p = nullptr, *zp = nullptr;
+    // slice-state form of pass 2: s'^T and W3^T fragments, valid after attention
+    // (not after a state injected as Z)
+    void *sfp = nullptr, *w3p = nullptr;
+    bool sf_ready = false;
     int64_t bytes = 0;
     // host bookkeeping
     std::vector<uint8_t> span_written;
@@ -422,9 +454,9 @@ const char *ts3_last_error(void) { return g_err.c_str(); }
 ts3_status ts3_state_free(ts3_state *st) {
     if (!st) return TS3_OK;
     hipError_t e = hipDeviceSynchronize();
-    void *bufs[] = {st->partials, st->runs, st->s_raw, st->dsum, st->s,    st->s1,   st->Z,
-                    st->b2s,      st->b3,   st->w2p,   st->zp,   st->bdZ,  st->bdsr, st->bdsT,
-                    st->bdd,      st->bdW2T, st->bdz};
+    void *bufs[] = {st->partials, st->runs, st->s_raw, st->dsum, st->s,    st->s1,    st->Z,
+                    st->b2s,      st->b3,   st->w2p,   st->zp,   st->bdZ,  st->bdsr,  st->bdsT,
+                    st->bdd,      st->bdW2T, st->bdz,  st->sfp,  st->w3p};
     for (void *b : bufs)
         if (b) (void)hipFree(b);
     if (st->ev_fork) (void)hipEventDestroy(st->ev_fork);
@@ -481,8 +513,13 @@ ts3_status ts3_state_create(const ts3_desc *desc, ts3_state **out) {
         {(void **)&st->bdsT, HM * d.C * 4},
         {(void **)&st->bdd, HM * 4},
         {(void **)&st->bdW2T, HM * d.C * 4},
+        // slice-state pass 2 (head width 16 only; empty otherwise)
+        {&st->sfp, d.H * 16 == d.C && st->k.pass2sf ? HM * 16 * 2 : 0},
+        {&st->w3p, d.H * 16 == d.C && st->k.pass2sf ? (int64_t)d.C * d.C * 2 : 0},
     };
+    if (d.H * 16 != d.C) st->k.pass2sf = nullptr;
     for (auto &r : reqs) {
+        if (r.bytes == 0) continue;
         hipError_t e = hipMalloc(r.p, (size_t)r.bytes);
         if (e != hipSuccess) {
             (void)hipGetLastError();
@@ -647,6 +684,17 @@ ts3_status ts3_token_attention(ts3_state *st, const ts3_weights *w, void *stream
     LAUNCH_CHECK("b3");
     ts3_status s = prep_z(st, hs);  // folds b3 into the prepared Z
     if (s != TS3_OK) return s;
+    st->sf_ready = false;
+    if (st->k.pass2sf && st->sfp && st->w3p) {
+        // operands of the slice-state pass 2: s'^T and W3^T fragments
+        const int64_t nsf = (int64_t)d.H * d.M * 16, nw3 = (int64_t)d.C * d.C;
+        hipLaunchKernelGGL(k_prep_sf<bf16_t>, dim3((unsigned)std::min<int64_t>((nsf + 255) / 256, 1024)), dim3(256),
+                           0, hs, st->s1, d.H, d.M, (bf16_t *)st->sfp);
+        hipLaunchKernelGGL(k_prep_w3f<bf16_t>, dim3((unsigned)std::min<int64_t>((nw3 + 255) / 256, 1024)),
+                           dim3(256), 0, hs, w->W3, d.C, (bf16_t *)st->w3p);
+        LAUNCH_CHECK("prep_sf");
+        st->sf_ready = true;
+    }
     st->phase = PH_ATTEND;
     return TS3_OK;
 }
@@ -666,7 +714,10 @@ ts3_status ts3_deslice(const ts3_state *st, const ts3_weights *w, const void *x_
     const ts3_desc &d = st->desc;
     if (n_chunk > ((int64_t)INT32_MAX) * 64) return fail(TS3_ERR_INVALID_ARG, "n_chunk too large for one launch");
     const hipError_t le =
-        st->k.pass2(x_chunk, n_chunk, d.H, d.C, d.M, st->w2p, st->b2s, st->zp, out_chunk, (hipStream_t)stream);
+        st->k.pass2sf && st->sf_ready
+            ? st->k.pass2sf(x_chunk, n_chunk, st->w2p, st->b2s, st->sfp, st->w3p, st->b3, out_chunk,
+                            (hipStream_t)stream)
+            : st->k.pass2(x_chunk, n_chunk, d.H, d.C, d.M, st->w2p, st->b2s, st->zp, out_chunk, (hipStream_t)stream);
     if (le != hipSuccess) return fail(TS3_ERR_HIP, "deslice LDS setup: %s", hipGetErrorString(le));
     LAUNCH_CHECK("deslice");
     return TS3_OK;
@@ -878,6 +929,7 @@ ts3_status ts3_state_set(ts3_state *st, const ts3_weights *w, int32_t which, con
     if (s == TS3_OK) s = prep_w2(st, w, hs);
     if (s != TS3_OK) return s;
     HIP_TRY(hipStreamSynchronize(hs));
+    st->sf_ready = false;  // an injected Z need not factor as s' W3: decode in the cached-Z form
     st->phase = PH_ATTEND;
     return TS3_OK;
 }
@@ -919,7 +971,7 @@ ts3_status scratch_base(void **out) {
 
 // Byte layout of the scratch array for one call (each region 256-aligned).
 struct ScratchLayout {
-    size_t partials, runs, s_raw, dsum, s, s1, Z, b2s, b3, w2p, zp, total;
+    size_t partials, runs, s_raw, dsum, s, s1, Z, b2s, b3, w2p, zp, sfp, w3p, total;
 };
 
 ScratchLayout scratch_layout(const ts3_desc &d, int64_t N, int64_t tile) {
@@ -947,6 +999,9 @@ ScratchLayout scratch_layout(const ts3_desc &d, int64_t N, int64_t tile) {
     find_any_kernels(d.io_dtype, d.C, d.M, &k);
     take(L.w2p, (size_t)w2p_elems(d) * esize);
     take(L.zp, (size_t)zp_elems(d, k.rt) * esize);
+    const bool sf = k.pass2sf && d.H * 16 == d.C;  // the slice-state pass 2, as for a state
+    take(L.sfp, sf ? (size_t)HM * 16 * 2 : 0);
+    take(L.w3p, sf ? (size_t)d.C * d.C * 2 : 0);
     L.total = at;
     return L;
 }
@@ -1009,6 +1064,12 @@ ts3_status ts3_layer_forward_noalloc(const ts3_desc *desc, const ts3_weights *w,
     st.b3 = (float *)(b + lay.b3);
     st.w2p = b + lay.w2p;
     st.zp = b + lay.zp;
+    if (st.k.pass2sf && d.H * 16 == d.C) {
+        st.sfp = b + lay.sfp;
+        st.w3p = b + lay.w3p;
+    } else {
+        st.k.pass2sf = nullptr;
+    }
     hipStream_t hs = (hipStream_t)stream;
     const int64_t Q = d.group_span;
     const int64_t E = st.E;
