@@ -189,10 +189,15 @@ __device__ __forceinline__ void interleave_chain() {
 // hold every later LDS access until it lands; callers track completion
 // themselves with wait_vmcnt.  M0 carries the LDS base; the kernels that use
 // this have no other M0 user (gfx950 LDS instructions do not read M0).
+// The compiler inserts no wait states for hazards inside assembly, so the
+// copies carry their own: one between the M0 write and the copy that reads
+// it, and, where the global base is a scalar operand that vector code may
+// have just written (v_readfirstlane), five before the copy reads it.
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
 __device__ __forceinline__ void dma16(const void *src, uint32_t lds_base) {
-    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds_base) : "memory", "m0");
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds_base)
+                 : "memory", "m0");
 }
 // The same copy with a wave-uniform global base and a per-lane 32-bit offset.
 template <int IMM> __device__ __forceinline__ void dma16s(uint32_t voff, const void *sbase, uint32_t lds_base) {
@@ -203,7 +208,7 @@ template <int IMM> __device__ __forceinline__ void dma16s(uint32_t voff, const v
     const uint64_t ub = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(b >> 32)) << 32) |
                         (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)b);
     sbase = (const void *)(uintptr_t)ub;
-    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1 offset:%3" ::"v"(voff), "s"(sbase),
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 3\n\tglobal_load_lds_dwordx4 %0, %1 offset:%3" ::"v"(voff), "s"(sbase),
                  "s"(lds_base), "n"(IMM)
                  : "memory", "m0");
 }

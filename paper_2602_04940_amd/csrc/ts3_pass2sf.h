@@ -31,7 +31,16 @@
 #include "ts3_pass2.h"
 #include "ts3_small.h"  // store_elem
 
+#include <type_traits>
+
 namespace ts3 {
+
+template <int I, int N, typename F> __device__ __forceinline__ void static_for(F &&f) {
+    if constexpr (I < N) {
+        f(std::integral_constant<int, I>{});
+        static_for<I + 1, N>(f);
+    }
+}
 
 template <int C, int M> struct Pass2SFCfg {
     static constexpr int DH = 16, H = C / DH;
@@ -40,8 +49,13 @@ template <int C, int M> struct Pass2SFCfg {
     static constexpr int W2_BYTES = H * MT * CK * 1024;  // W2'^T fragments, all heads
     static constexpr int SF_BYTES = H * KM * 1024;       // s'^T fragments, all heads
     static constexpr int B2_BYTES = H * M * 4;           // b2' = b2 * log2(e) / tau
-    static constexpr int B3_BYTES = C * 4;
-    static constexpr int LDS_BYTES = W2_BYTES + SF_BYTES + B2_BYTES + B3_BYTES;
+    static constexpr int B3_BYTES = C * 4 <= 1024 ? 1024 : C * 4;
+    // the small operands first, so that their LDS addresses stay within the
+    // 64 KB reach of an instruction's immediate offset from one base
+    static constexpr int B2_AT = 0, B3_AT = (B2_BYTES + 1023) / 1024 * 1024, SF_AT = B3_AT + B3_BYTES,
+                         W2_AT = SF_AT + SF_BYTES;
+    static constexpr int LDS_BYTES = W2_AT + W2_BYTES;
+    static_assert(W2_AT % 1024 == 0, "W2' fragments 1 KB aligned");
     static constexpr int NXLOAD = PT * CK;  // x fragments of a wave block: one per head
     static constexpr int NW3 = CK * CT;     // W3^T fragments (K steps outermost)
     static constexpr int W3_AHEAD = 8;      // W3^T fragments in flight
@@ -176,10 +190,9 @@ __global__ __launch_bounds__(512, 1) void k_deslice_sf(const bf16_t *__restrict_
     constexpr int H = Cfg::H, CT = Cfg::CT, MT = Cfg::MT, CK = Cfg::CK, KM = Cfg::KM, PT = Cfg::PT;
     constexpr int WAVES = Cfg::WAVES, NW3 = Cfg::NW3, AHEAD = Cfg::W3_AHEAD;
     __shared__ __attribute__((aligned(1024))) unsigned char lds[Cfg::LDS_BYTES];
-    const T *const w2l = reinterpret_cast<const T *>(lds);
-    const T *const sfl = reinterpret_cast<const T *>(lds + Cfg::W2_BYTES);
-    float *const b2l = reinterpret_cast<float *>(lds + Cfg::W2_BYTES + Cfg::SF_BYTES);
-    float *const b3l = reinterpret_cast<float *>(lds + Cfg::W2_BYTES + Cfg::SF_BYTES + Cfg::B2_BYTES);
+    const T *const sfl = reinterpret_cast<const T *>(lds + Cfg::SF_AT);
+    float *const b2l = reinterpret_cast<float *>(lds + Cfg::B2_AT);
+    float *const b3l = reinterpret_cast<float *>(lds + Cfg::B3_AT);
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
@@ -191,9 +204,9 @@ __global__ __launch_bounds__(512, 1) void k_deslice_sf(const bf16_t *__restrict_
     {   // resident operands: W2' by direct copies, the small ones through registers
         const unsigned char *src = reinterpret_cast<const unsigned char *>(w2p);
         for (int b = wave * 64; b < Cfg::W2_BYTES / 16; b += WAVES * 64)
-            dma16(src + (b + lane) * 16, lds_addr(lds + b * 16));
+            dma16(src + (b + lane) * 16, lds_addr(lds + Cfg::W2_AT + b * 16));
         const uint4 *s4 = reinterpret_cast<const uint4 *>(sf);
-        uint4 *d4 = reinterpret_cast<uint4 *>(lds + Cfg::W2_BYTES);
+        uint4 *d4 = reinterpret_cast<uint4 *>(lds + Cfg::SF_AT);
         for (int i = threadIdx.x; i < Cfg::SF_BYTES / 16; i += 64 * WAVES) d4[i] = s4[i];
         for (int i = threadIdx.x; i < H * M; i += 64 * WAVES) b2l[i] = b2s[i];
         for (int i = threadIdx.x; i < C; i += 64 * WAVES) b3l[i] = b3[i];
@@ -210,9 +223,16 @@ __global__ __launch_bounds__(512, 1) void k_deslice_sf(const bf16_t *__restrict_
     };
     const int64_t pw = (int64_t)blockIdx.x * Cfg::POINTS_PER_WG + wave * (16 * PT);
     const int64_t bstride = (int64_t)gridDim.x * Cfg::POINTS_PER_WG;
-    Frag<T> xb[PT][CK], xn[PT][CK];
+    Frag<T> xb[PT][CK];
 #pragma unroll
     for (int j = 0; j < Cfg::NXLOAD; ++j) load_xfrag(pw, j, xb);
+    // The first block's x is waited for here, where the compiler sees it:
+    // otherwise its wait for these loads would sit at the top of the block
+    // loop and hold every later block until the previous block's stores retire.
+#pragma unroll
+    for (int pt = 0; pt < PT; ++pt)
+#pragma unroll
+        for (int kc = 0; kc < CK; ++kc) asm volatile("" : "+v"(xb[pt][kc].v));
     wait_vmcnt<0>();  // this wave's direct copies (the compiler does not count them)
     __syncthreads();  // every wave's copies and LDS stores visible
     uint64_t failed = 0;  // bit i: block i left the fast path
@@ -220,7 +240,6 @@ __global__ __launch_bounds__(512, 1) void k_deslice_sf(const bf16_t *__restrict_
 
     for (int i = 0; i < iters; ++i) {
         const int64_t p0 = pw + (int64_t)i * bstride;
-        const bool has_next = i + 1 < iters;
         bool ok = true;
         Frag<T> ub[CK][PT];  // u of head pairs: the B fragments of the Linear3 product
         f32x4 Uprev[PT];
@@ -252,15 +271,22 @@ __global__ __launch_bounds__(512, 1) void k_deslice_sf(const bf16_t *__restrict_
             {
                 constexpr int NSTEP = MT * CK, DIST = 2, EPS = (4 * PT) / CK;
                 static_assert((4 * PT) % CK == 0, "exp2 spread evenly over a tile's K steps");
-                const T *wh = w2l + (size_t)h * MT * CK * 512 + lane * 8;
+                // The head's fragments from one base register plus immediate
+                // offsets; the base is opaque to the compiler, which would
+                // otherwise hold one address register per fragment of the launch.
+                uint32_t hoff = (uint32_t)(h * MT * CK * 1024 + lane * 16);
+                asm volatile("" : "+v"(hoff));
+                auto w2frag = [&](int s, Frag<T> &f) {
+                    f.v = *reinterpret_cast<const bf16x8 *>(lds + Cfg::W2_AT + hoff + s * 1024);
+                };
                 Frag<T> a[4];
 #pragma unroll
-                for (int s = 0; s < DIST; ++s) load8(a[s], wh + s * 512);
+                for (int s = 0; s < DIST; ++s) w2frag(s, a[s]);
 #pragma unroll
                 for (int s = 0; s < NSTEP; ++s) {
                     const int mt = s / CK, kc = s % CK;
                     __builtin_amdgcn_sched_barrier(0);
-                    if (s + DIST < NSTEP) load8(a[(s + DIST) & 3], wh + (s + DIST) * 512);
+                    if (s + DIST < NSTEP) w2frag(s + DIST, a[(s + DIST) & 3]);
 #pragma unroll
                     for (int pt = 0; pt < PT; ++pt) mma(L[mt][pt], a[s & 3], xb[pt][kc]);
                     if (mt > 0)
@@ -271,11 +297,6 @@ __global__ __launch_bounds__(512, 1) void k_deslice_sf(const bf16_t *__restrict_
                     for (int q = 0; q < PT || q < EPS; ++q) {
                         if (q < PT) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
                         if (mt > 0 && q < EPS) __builtin_amdgcn_sched_group_barrier(0x400, 1, 0);
-                    }
-                    // This head's x fragment of the next block, after the first tile.
-                    if (s == CK - 1 && has_next) {
-                        __builtin_amdgcn_sched_barrier(0);
-                        load_xfrag(p0 + bstride, h, xn);
                     }
                 }
                 __builtin_amdgcn_sched_barrier(0);
@@ -319,37 +340,51 @@ __global__ __launch_bounds__(512, 1) void k_deslice_sf(const bf16_t *__restrict_
             for (int pt = 0; pt < PT; ++pt) O[ct][pt] = b;
         }
         {
-            const T *wl = w3f + lane * 8;
+            // the kernel argument as the scalar base plus a 32-bit offset, so
+            // the loads need no per-fragment 64-bit address registers
+            // AHEAD fragments in flight, and the next block's x issued right
+            // after the last fragment, so that no fragment's wait covers it
+            // (in the last block x is reloaded anyway, clamped rows).  Each
+            // load is the scalar base (the kernel argument) plus a 32-bit
+            // lane offset plus an immediate, four fragments per offset.
+            const unsigned char *w3b = reinterpret_cast<const unsigned char *>(w3f);
+            const uint32_t voff = (uint32_t)lane * 16u;
+            auto w3frag = [&](int q, Frag<T> &f) {
+                f.v = *reinterpret_cast<const bf16x8 *>(w3b + (uint32_t)(voff + 4096u * (q / 4)) + (q % 4) * 1024);
+            };
             Frag<T> a[AHEAD];
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-            for (int q = 0; q < AHEAD; ++q) load8(a[q], wl + q * 512);
-#pragma unroll
-            for (int q = 0; q < NW3; ++q) {
-                const int kk = q / CT, ct = q % CT;
+            for (int q = 0; q < AHEAD; ++q) w3frag(q, a[q]);
+            static_for<0, NW3>([&](auto qc) {
+                constexpr int q = decltype(qc)::value, kk = q / CT, ct = q % CT;
 #pragma unroll
                 for (int pt = 0; pt < PT; ++pt) mma(O[ct][pt], a[q % AHEAD], ub[kk][pt]);
-                if (q + AHEAD < NW3) load8(a[q % AHEAD], wl + (q + AHEAD) * 512);
-            }
+                __builtin_amdgcn_sched_barrier(0);
+                if constexpr (q + AHEAD < NW3) w3frag(q + AHEAD, a[q % AHEAD]);
+                if constexpr (q + AHEAD == NW3 - 1) {
+#pragma unroll
+                    for (int j = 0; j < Cfg::NXLOAD; ++j) load_xfrag(p0 + bstride, j, xb);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            });
         }
         if (!ok) failed |= 1ull << i;
-        if (has_next) {
-            // every block but a workgroup's last is full: unconditional stores
+        // The same stores for every block (one path through the loop, so the
+        // compiler's waits at its top need not allow for a block without
+        // them): a row past the end computed the last row's x, so it writes
+        // the last row's values to the last row.  A block that left the fast
+        // path is rewritten below.
 #pragma unroll
-            for (int k = 0; k < CT / 2; ++k)
+        for (int k = 0; k < CT / 2; ++k)
 #pragma unroll
-                for (int pt = 0; pt < PT; ++pt) {
-                    const f32x4 &u = O[2 * k][pt], &v = O[2 * k + 1][pt];
-                    *reinterpret_cast<bf16x8 *>(out + (size_t)(p0 + pt * 16 + li) * C + 32 * k + 8 * g) =
-                        bf16x8{(__bf16)u[0], (__bf16)u[1], (__bf16)u[2], (__bf16)u[3],
-                               (__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
-                }
-#pragma unroll
-            for (int pt = 0; pt < PT; ++pt)
-#pragma unroll
-                for (int kc = 0; kc < CK; ++kc) xb[pt][kc] = xn[pt][kc];
-        } else if (ok) {
-            store_rows<T, CT, PT, C>(O, out, p0, n, g, li);  // the last block, possibly partial
-        }
+            for (int pt = 0; pt < PT; ++pt) {
+                const f32x4 &u = O[2 * k][pt], &v = O[2 * k + 1][pt];
+                const int64_t p = p0 + pt * 16 + li;
+                *reinterpret_cast<bf16x8 *>(out + (size_t)(p < n ? p : n - 1) * C + 32 * k + 8 * g) =
+                    bf16x8{(__bf16)u[0], (__bf16)u[1], (__bf16)u[2], (__bf16)u[3],
+                           (__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
+            }
     }
     // Rare: blocks whose exp2 sums left the safe window, redone from
     // global-memory operands with the max-shifted softmax, 16 points at a time.
