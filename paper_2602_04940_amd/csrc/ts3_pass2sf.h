@@ -237,6 +237,8 @@ __global__ __launch_bounds__(512, 1) void k_deslice_sf(const bf16_t *__restrict_
     __syncthreads();  // every wave's copies and LDS stores visible
     uint64_t failed = 0;  // bit i: block i left the fast path
     f32x4 O[CT][PT];
+    Frag<T> ones;
+    ones8(ones);
 
     for (int i = 0; i < iters; ++i) {
         const int64_t p0 = pw + (int64_t)i * bstride;
@@ -255,18 +257,14 @@ __global__ __launch_bounds__(512, 1) void k_deslice_sf(const bf16_t *__restrict_
             Frag<T> sa[KM];
 #pragma unroll
             for (int km = 0; km < KM; ++km) sa[km].v = *reinterpret_cast<const bf16x8 *>(sfl + ((h * KM + km) * 64 + lane) * 8);
-            // Slice tiles outermost: the exp2 of tile mt-1 (and its row sums)
-            // ride between tile mt's MFMAs; the W2' fragment of step i+2 is
-            // read while step i's MFMAs run.
-            float esum[PT];
-#pragma unroll
-            for (int pt = 0; pt < PT; ++pt) esum[pt] = 0.f;
+            // Slice tiles outermost: the exp2 of tile mt-1 rides between tile
+            // mt's MFMAs; the W2' fragment of step i+2 is read while step i's
+            // MFMAs run.
             auto exp_at = [&](int mt, int e) {
                 const int pt = e / 4, r = e % 4;
                 float v = fast_exp2(L[mt][pt][r]);
                 asm volatile("" : "+v"(v));
                 L[mt][pt][r] = v;
-                esum[pt] += v;
             };
             {
                 constexpr int NSTEP = MT * CK, DIST = 2, EPS = (4 * PT) / CK;
@@ -303,23 +301,28 @@ __global__ __launch_bounds__(512, 1) void k_deslice_sf(const bf16_t *__restrict_
 #pragma unroll
                 for (int e = 0; e < 4 * PT; ++e) exp_at(MT - 1, e);
             }
+            // The unnormalised exp2 terms e go into the products: u_h is
+            // linear in the weights, so u_h = (s'_h^T e) / sum(e), and the row
+            // sums come from the same products with an all-ones A operand
+            // (every output row of that tile is the sum over the slices).
+            // Both sums use the same bf16-rounded e, so the weights that u
+            // averages with sum to one exactly.
             Frag<T> wf[PT][KM];
-            {
-                bool okk = true;
 #pragma unroll
-                for (int pt = 0; pt < PT; ++pt) {
-                    const float sm = xrow_sum(esum[pt]);
-                    okk = okk && softmax_sum_ok(sm);
-                    pack_weights<T, MT, PT, KM>(L, pt, fast_rcp(sm), wf);
-                }
-                ok = !__any(!okk) && ok;
-            }
-            // u_h = s'_h^T w: two products per point tile.
+            for (int pt = 0; pt < PT; ++pt) pack_weights<T, MT, PT, KM>(L, pt, 1.0f, wf);
+            bool okk = true;
 #pragma unroll
             for (int pt = 0; pt < PT; ++pt) {
-                f32x4 U{0.f, 0.f, 0.f, 0.f};
+                f32x4 U{0.f, 0.f, 0.f, 0.f}, S{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int km = 0; km < KM; ++km) mma(U, sa[km], wf[pt][km]);
+                for (int km = 0; km < KM; ++km) {
+                    mma(U, sa[km], wf[pt][km]);
+                    mma(S, ones, wf[pt][km]);
+                }
+                okk = okk && softmax_sum_ok(S[0]);
+                const float inv = fast_rcp(S[0]);
+#pragma unroll
+                for (int r = 0; r < 4; ++r) U[r] *= inv;
                 if (h & 1) {
                     ub[h >> 1][pt].set2(0, Uprev[pt][0], Uprev[pt][1]);
                     ub[h >> 1][pt].set2(2, Uprev[pt][2], Uprev[pt][3]);
@@ -329,6 +332,7 @@ __global__ __launch_bounds__(512, 1) void k_deslice_sf(const bf16_t *__restrict_
                     Uprev[pt] = U;
                 }
             }
+            ok = !__any(!okk) && ok;
         }
         // out = b3 + u W3: W3^T fragments streamed from global memory (L2),
         // K steps outermost so that consecutive MFMAs are independent.
