@@ -16,14 +16,14 @@ def _matvec_row(row, W, col0, ncol):
     return [sum(row[k] * W[k][col0 + j] for k in range(len(row))) for j in range(ncol)]
 
 
-def layer_forward_loops(x, W, H, M, inv_tau, eps=0.0):
+def slice_tokens_loops(x, W, H, M, inv_tau, eps=0.0):
+    """Slice weights w[i][h][m] and slice tokens s[h][m][k] of Eq. (1)-(2):
+    project each point with Linear1, then take each slice's weighted mean."""
     x = [list(map(float, r)) for r in x]
     N, C = len(x), len(x[0])
     dh = C // H
     W2 = W["W2"].tolist(); b2 = W["b2"].tolist()
     W1 = W["W1"].tolist(); b1 = W["b1"].tolist()
-    Wq = W["Wq"].tolist(); Wk = W["Wk"].tolist(); Wv = W["Wv"].tolist()
-    W3 = W["W3"].tolist(); b3 = W["b3"].tolist()
 
     # slice weights w[i][h][m]
     w = []
@@ -50,6 +50,15 @@ def layer_forward_loops(x, W, H, M, inv_tau, eps=0.0):
             for k in range(dh):
                 num = sum(w[i][h][m] * xp[i][h][k] for i in range(N))
                 s[h][m][k] = num / den if den > 0 else 0.0
+    return w, s
+
+
+def layer_forward_loops(x, W, H, M, inv_tau, eps=0.0):
+    N, C = len(x), len(x[0])
+    dh = C // H
+    w, s = slice_tokens_loops(x, W, H, M, inv_tau, eps)
+    Wq = W["Wq"].tolist(); Wk = W["Wk"].tolist(); Wv = W["Wv"].tolist()
+    W3 = W["W3"].tolist(); b3 = W["b3"].tolist()
 
     # per-head attention among M tokens
     s1 = [[[0.0] * dh for _ in range(M)] for _ in range(H)]

@@ -23,7 +23,9 @@ section 3.2, "Faster slice and deslice"):
     property here, not the way the state is defined.
 The reordered form is also exposed in pieces (``slice_accumulate`` for any
 part of the mesh, ``token_side`` ... ``deslice``) so each GPU entry point has
-a matching oracle step.
+a matching oracle step; ``projected_accumulate`` / ``projected_finalize`` give
+the state from sums taken after Linear1 (the order of Eq. (2)), for GPU paths
+that accumulate projected sums.
 
 Parity pins: every function here is checked in ``tests/test_oracle.py``
 against brute-force loops, closed forms (M = 1, 1/tau = 0, one-hot slices),
@@ -116,6 +118,31 @@ def slice_finalize(s_raw, d, W1, b1, H: int, eps: float = 0.0):
     W1, b1 = _f64(W1), _f64(b1)
     return np.stack([mean[h] @ W1[:, h * dh:(h + 1) * dh] + b1[h * dh:(h + 1) * dh]
                      for h in range(H)])
+
+
+def projected_accumulate(x_tile, W2, b2, W1, H: int, M: int, inv_tau: float):
+    """One tile's contribution with Linear1 applied per point first, the order
+    of Eq. (2): each point's head-h projection f_ih = x_i W1[:, h*dh:(h+1)*dh]
+    (without b1) is summed with its slice weights, t^(t) = sum_i w_ih f_ih
+    [H, M, dh], with d^(t) = sum_i w_i [H, M].  Linear1 is linear, so
+    t = s_raw W1_h per head: the sums of Eq. (4) taken after the projection."""
+    x_tile = _f64(x_tile)
+    N, C = x_tile.shape
+    dh = C // H
+    w = slice_weights(x_tile, W2, b2, H, M, inv_tau)
+    f = (x_tile @ _f64(W1)).reshape(N, H, dh)
+    return np.einsum("nhm,nhj->hmj", w, f), w.sum(axis=0)
+
+
+def projected_finalize(t_raw, d, b1, H: int, eps: float = 0.0):
+    """s = d^-1 t + b1 per head from projected sums: the same s as
+    ``slice_finalize`` (the mean commutes with the bias-free projection, and
+    b1 is added once per slice token); an empty slice gives s = b1."""
+    t_raw, d = _f64(t_raw), _f64(d)
+    dh = t_raw.shape[2]
+    den = (d + eps)[:, :, None]
+    mean = np.divide(t_raw, den, out=np.zeros_like(t_raw), where=den > 0)
+    return mean + _f64(b1).reshape(H, 1, dh)
 
 
 def linear3_tokens(s1, W3) -> np.ndarray:

@@ -2,9 +2,10 @@
 
 TEST INFRASTRUCTURE (see ``physics_attention.py``): only the tests, the smoke
 check and the benchmark's CPU baseline use it.  It adds no arithmetic of its
-own.  Workers run the oracle's ``slice_accumulate`` on one tile, or its
-``deslice`` on one chunk.  The parent adds the tile terms in tile-index order
-(Eq. (4): the state's sums are additive over parts of the mesh), in the same
+own.  Workers run the oracle's ``slice_accumulate`` (or
+``projected_accumulate``) on one tile, or its ``deslice`` on one chunk.  The
+parent adds the tile terms in tile-index order (Eq. (4): the state's sums
+are additive over parts of the mesh), in the same
 order and from the same zero start as ``build_state``, so both give bitwise
 equal results.  It then runs the token side (``token_side``) once.
 
@@ -30,6 +31,11 @@ def _init():
 def _tile_sum(args):
     x, W2, b2, H, M, inv_tau = args
     return PA.slice_accumulate(np.asarray(x, dtype=np.float64), W2, b2, H, M, inv_tau)
+
+
+def _tile_psum(args):
+    x, W2, b2, W1, H, M, inv_tau = args
+    return PA.projected_accumulate(np.asarray(x, dtype=np.float64), W2, b2, W1, H, M, inv_tau)
 
 
 def _tile_decode(args):
@@ -80,6 +86,14 @@ class OraclePool:
     def sums(self, parts, W2, b2, H: int, M: int, inv_tau: float):
         """[(s_raw, d)] of ``slice_accumulate`` over each point set in ``parts``."""
         return list(self.ex.map(_tile_sum, [(self._pack(p), W2, b2, H, M, inv_tau) for p in parts]))
+
+    def projected_sums(self, parts, W2, b2, W1, H: int, M: int, inv_tau: float):
+        """[(t_raw, d)] of ``projected_accumulate`` over each point set in ``parts``."""
+        return list(self.ex.map(_tile_psum, [(self._pack(p), W2, b2, W1, H, M, inv_tau) for p in parts]))
+
+    def projected_tile_sums(self, x, W2, b2, W1, H: int, M: int, inv_tau: float, tile: int):
+        """[(t_raw_t, d_t)] for the tiles [t0, t0 + tile) of x, in tile order."""
+        return self.projected_sums([x[t0:t0 + tile] for t0 in range(0, len(x), tile)], W2, b2, W1, H, M, inv_tau)
 
     def state(self, x, W, H: int, M: int, inv_tau: float, tile: int = 65536, eps: float = 0.0):
         """The oracle's ``build_state(x, W, H, M, inv_tau, tile, eps)``, tiles in parallel."""

@@ -15,7 +15,7 @@ import pytest
 
 import oracle
 import oracle.physics_attention as PA
-from oracle.brute import layer_forward_loops
+from oracle.brute import layer_forward_loops, slice_tokens_loops
 from ts3_synth import WORKLOADS, make_weights
 from ts3_synth.workloads import small_features
 
@@ -83,6 +83,43 @@ def check_brute():
 
 def test_brute_force_loops_match():
     check_brute()
+
+
+# ------------------------------------- projected sums (Linear1 before the sum)
+
+def check_projected():
+    """State from sums taken after Linear1: the hand-worked s of the fixture,
+    the loop form's slice tokens, and the closed form sum_m t[h, m] =
+    (sum_i x_i) W1_h (each point's weights sum to one per head)."""
+    g, x, W = load_golden()
+    H, M, it = g["H"], g["M"], g["inv_tau"]
+    t, d = oracle.projected_accumulate(x, W["W2"], W["b2"], W["W1"], H, M, it)
+    np.testing.assert_allclose(oracle.projected_finalize(t, d, W["b1"], H), _arr(g["expect"]["s"]),
+                               rtol=1e-6, atol=1e-7)
+    for (N, C, H, M, seed) in [(9, 4, 1, 3, 1), (16, 8, 2, 3, 2), (11, 6, 3, 2, 3)]:
+        x, W = _rand_case(N, C, H, M, seed)
+        _, s_ref = slice_tokens_loops(x, W, H, M, 1.7)
+        t, d = oracle.projected_accumulate(x, W["W2"], W["b2"], W["W1"], H, M, 1.7)
+        np.testing.assert_allclose(oracle.projected_finalize(t, d, W["b1"], H), np.array(s_ref), rtol=0, atol=1e-12)
+        dh = C // H
+        col = x.sum(axis=0) @ W["W1"].astype(np.float64)
+        for h in range(H):
+            np.testing.assert_allclose(t[h].sum(axis=0), col[h * dh:(h + 1) * dh], rtol=0, atol=1e-12)
+
+
+def test_projected_sums_give_the_same_state():
+    check_projected()
+
+
+def test_projected_sums_are_additive_and_empty_slices_give_b1():
+    x, W = _rand_case(N=500, C=16, H=4, M=6, seed=13)
+    t, d = oracle.projected_accumulate(x, W["W2"], W["b2"], W["W1"], 4, 6, 2.0)
+    parts = [oracle.projected_accumulate(x[i:i + 77], W["W2"], W["b2"], W["W1"], 4, 6, 2.0)
+             for i in range(0, 500, 77)]
+    np.testing.assert_allclose(sum(p[0] for p in parts), t, rtol=1e-13, atol=1e-13 * np.abs(t).max())
+    np.testing.assert_allclose(sum(p[1] for p in parts), d, rtol=1e-13)
+    s = oracle.projected_finalize(np.zeros_like(t), np.zeros_like(d), W["b1"], 4)
+    np.testing.assert_array_equal(s, np.broadcast_to(W["b1"].astype(np.float64).reshape(4, 1, 4), s.shape))
 
 
 # ------------------------------------------------------ invariants of Eq. (1)
@@ -247,7 +284,8 @@ def test_workload_inputs_are_deterministic_and_normalised():
 def _mutants():
     """Plausible oracle mistakes; each must be caught by some pin."""
     orig = {n: getattr(PA, n) for n in ("slice_weights", "slice_finalize", "linear3_tokens",
-                                          "token_attention", "deslice", "slice_accumulate")}
+                                          "token_attention", "deslice", "slice_accumulate",
+                                          "projected_accumulate", "projected_finalize")}
 
     def sw_wrong_axis(x, W2, b2, H, M, inv_tau):
         lg = (np.asarray(x, float) @ W2.astype(float) + b2).reshape(len(x), H, M) * inv_tau
@@ -299,7 +337,22 @@ def _mutants():
         s_raw, d = orig["slice_accumulate"](x_tile, W2, b2, H, M, inv_tau)
         return s_raw, np.full_like(d, len(x_tile) / M)
 
+    def pacc_bias_in_sum(x_tile, W2, b2, W1, H, M, inv_tau):
+        t, d = orig["projected_accumulate"](x_tile, W2, b2, W1, H, M, inv_tau)
+        return t + 0.5 * d[:, :, None], d
+
+    def pacc_head_block(x_tile, W2, b2, W1, H, M, inv_tau):
+        C = W1.shape[1]
+        perm = np.roll(np.arange(C), C // H)  # head h meets head h-1's columns
+        return orig["projected_accumulate"](x_tile, W2, b2, np.asarray(W1)[:, perm], H, M, inv_tau)
+
+    def pfin_no_b1(t_raw, d, b1, H, eps=0.0):
+        return orig["projected_finalize"](t_raw, d, np.zeros_like(b1), H, eps)
+
     return {
+        "projected sums carry a bias": ("projected_accumulate", pacc_bias_in_sum),
+        "projected with another head's W1 block": ("projected_accumulate", pacc_head_block),
+        "b1 dropped from projected state": ("projected_finalize", pfin_no_b1),
         "softmax over heads": ("slice_weights", sw_wrong_axis),
         "temperature multiplied": ("slice_weights", sw_tau_mult),
         "b2 dropped": ("slice_weights", sw_no_bias),
@@ -316,7 +369,7 @@ def _mutants():
 
 def _pins_pass():
     checks = [check_golden, check_brute, check_closed_forms, check_one_hot, check_orig_equals_fast,
-              check_attention_library]
+              check_attention_library, check_projected]
     for c in checks:
         try:
             c()
