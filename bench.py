@@ -131,15 +131,22 @@ def pmc_driver(points: int, workloads=("layer",)):
 
 # Kernels whose counters are summarised: name prefix -> (points per dispatch,
 # matrix flop per point that the kernel executes, algorithmic HBM bytes per
-# point, peak TFLOP/s of its matrix dtype).  Forward passes execute 4*C*H*M
-# (logits and one contraction); the backward's dZ kernel 4, its dx kernel 10
-# and its dW2 kernel 2 (x C*H*M), of which the backward as a whole needs 14.
-# The dx kernel writes dz (H*M floats per point), which the dW2 kernel reads.
+# point, peak TFLOP/s of its matrix dtype).  The first forward kernels execute
+# 4*C*H*M (logits and one contraction).  The projected pass 1 executes
+# 2*(C*H*M + 2*C*C + 4*M*C): logits, x W1 per head (rounded W1 and its
+# remainder), the weighted sums of the projected rows (rounded value and
+# remainder), their weight sums and the softmax row sums; the slice-state
+# pass 2 executes 2*(C*H*M + 2*M*C + C*C): logits, w s' per head, the row
+# sums, and Linear3.  The backward's dZ kernel 4, its dx kernel 10 and its dW2
+# kernel 2 (x C*H*M), of which the backward as a whole needs 14.  The dx
+# kernel writes dz (H*M floats per point), which the dW2 kernel reads.
 SQ_COUNTERS = ("SQ_INSTS_MFMA SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU SQ_INSTS_VALU_TRANS_F32 "
                "SQ_INSTS_LDS SQ_LDS_BANK_CONFLICT SQ_LDS_IDX_ACTIVE SQ_BUSY_CYCLES GRBM_GUI_ACTIVE")
 COUNTER_KERNELS = {
     "k_slice_accumulate_pc<": (1_000_000, 4 * 128 * 512, 256, PEAK_BF16_TFLOPS),
     "k_deslice_w8<": (1_000_000, 4 * 128 * 512, 512, PEAK_BF16_TFLOPS),
+    "k_slice_accumulate_pcp<": (1_000_000, 2 * (128 * 512 + 2 * 128 * 128 + 4 * 64 * 128), 256, PEAK_BF16_TFLOPS),
+    "k_deslice_sf<": (1_000_000, 2 * (128 * 512 + 2 * 64 * 128 + 128 * 128), 512, PEAK_BF16_TFLOPS),
     "k_slice_accumulate_pcw<": (1_000_000, 4 * 256 * 512, 512, PEAK_BF16_TFLOPS),
     "k_deslice_pc<": (1_000_000, 4 * 256 * 512, 1024, PEAK_BF16_TFLOPS),
     "k_mlp_residual_pc<": (1_000_000, 4 * 256 * 1024, 1536, PEAK_BF16_TFLOPS),
@@ -299,7 +306,7 @@ def summarize_traffic(fetch_dir: str, write_dir: str, command: str):
         factor = CAL_BYTES / (float(cal["Counter_Value"]) * 1024.0)
         out.setdefault("calibration", {})[name] = {"copy_bytes": CAL_BYTES, "counter_kib": float(cal["Counter_Value"]),
                                                   "bytes_per_counted_byte": factor}
-        for kname in ("k_slice_accumulate_pc", "k_deslice_w8"):
+        for kname in ("k_slice_accumulate_pc", "k_slice_accumulate_pcp", "k_deslice_w8", "k_deslice_sf"):
             vals = [float(r["Counter_Value"]) for r in rs if kname + "<" in r["Kernel_Name"]]
             per.setdefault(kname, {})[name] = (sum(vals) / len(vals), len(vals), factor)
     for kname, d in per.items():
@@ -344,7 +351,14 @@ def cpu_baseline_and_parity(x_dev, W, lw, wl, sample):
                           max_points=sample) as layer:
         out = layer.forward(lw, xs, tile=wl.tile, chunk=wl.chunk)
         torch.cuda.synchronize()
-        g_sr, g_d, g_z = layer.get(L.TS3_S_RAW), layer.get(L.TS3_D), layer.get(L.TS3_ZP)
+        proj = layer.projected()
+        g_sr, g_d, g_z = layer.get(L.TS3_T_RAW if proj else L.TS3_S_RAW), layer.get(L.TS3_D), layer.get(L.TS3_ZP)
+    if proj:  # the state keeps sums of projected rows: compare with the oracle's
+        with OraclePool() as pool:
+            parts = pool.projected_tile_sums(x64, W["W2"], W["b2"], W["W1"], wl.H, wl.M, it, 65536)
+        ref_sums = sum((t[0] for t in parts), np.zeros((wl.H, wl.M, wl.dh)))
+    else:
+        ref_sums = st["s_raw"]
     got = out.float().cpu().numpy().astype(np.float64)
 
     def rel(a, b):
@@ -356,12 +370,12 @@ def cpu_baseline_and_parity(x_dev, W, lw, wl, sample):
     rn = np.linalg.norm(ref, axis=1)
     row = np.linalg.norm(got - ref, axis=1) / np.maximum(rn, np.sqrt((rn ** 2).mean()))
     HM = wl.H * wl.M
-    tok = np.linalg.norm((g_sr - st["s_raw"]).reshape(HM, -1), axis=1) / np.linalg.norm(
-        st["s_raw"].reshape(HM, -1), axis=1)
+    tok = np.linalg.norm((g_sr - ref_sums).reshape(HM, -1), axis=1) / np.linalg.norm(
+        ref_sums.reshape(HM, -1), axis=1)
     parity = {"sample": f"first {sample} points as their own mesh, group span {wl.group_span}, "
                         f"{wl.tile}-point tiles and chunks",
               "bar": 0.02, "out_rel_l2": rel(got, ref), "out_worst_256_block": float(np.sqrt(d2 / r2).max()),
-              "out_worst_row": float(row.max()), "s_raw_worst_token": float(tok.max()),
+              "out_worst_row": float(row.max()), ("t_raw" if proj else "s_raw") + "_worst_token": float(tok.max()),
               "d_worst_rel": float((np.abs(g_d - st["d"]) / st["d"]).max()), "Z_rel_l2": rel(g_z, st["Z"])}
     parity["pass"] = all(v <= 0.02 for k, v in parity.items() if k not in ("sample", "bar"))
     return base, parity
@@ -723,19 +737,35 @@ def main():
     t_p1, t_mid, t_p2 = (ev[i].elapsed_time(ev[i + 1]) for i in range(3))
     log(f"pass1 {t_p1:.3f} ms ({ntile} launches), state {t_mid:.3f} ms, pass2 {t_p2:.3f} ms ({nchunk} launches)")
 
-    flop_per_point = 4 * wl.C * wl.H * wl.M        # logits + contraction, per pass
+    # Algorithmic flop per point and pass (Table 2's N-terms): the logits
+    # 2*C*H*M and one contraction with the slices 2*H*M*C.  The kernels reach
+    # the same result with fewer products by reassociating the linear steps
+    # (projected pass 1, slice-state pass 2); what they execute is reported
+    # beside it.
+    C, H, M = wl.C, wl.H, wl.M
+    flop_per_point = 4 * C * H * M
+    proj = layer.projected()
+    sf = H * 16 == C  # the slice-state pass 2 serves head width 16
+    p1 = ("k_slice_accumulate_pcp", 2 * (C * H * M + 2 * C * C + 4 * M * C)) if proj else \
+        ("k_slice_accumulate_pc", flop_per_point)
+    p2 = ("k_deslice_sf", 2 * (C * H * M + 2 * M * C + C * C)) if sf else ("k_deslice_w8", flop_per_point)
     if t_p1 >= t_p2:
-        kname, t_launch, nl = "k_slice_accumulate_pc", t_p1 / ntile, ntile
+        (kname, exec_pt), t_launch, nl = p1, t_p1 / ntile, ntile
     else:
-        kname, t_launch, nl = "k_deslice_w8", t_p2 / nchunk, nchunk
+        (kname, exec_pt), t_launch, nl = p2, t_p2 / nchunk, nchunk
     pts_launch = min(wl.tile, N)
     achieved = flop_per_point * pts_launch / (t_launch * 1e-3) / 1e12
+    executed = exec_pt * pts_launch / (t_launch * 1e-3) / 1e12
     traffic = measured_traffic(kname, pts_launch)
     layer_tflops = 2 * flop_per_point * N / (ms * 1e-3) / 1e12   # both passes over the timed step
+    layer_exec = (p1[1] + p2[1]) * N / (ms * 1e-3) / 1e12
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic, "kernel": kname,
                 "launch_ms": round(t_launch, 4), "launches": nl,
-                "layer_achieved": round(layer_tflops, 2), "layer_frac": round(layer_tflops / PEAK_BF16_TFLOPS, 4)}
+                "executed_achieved": round(executed, 2), "executed_frac": round(executed / PEAK_BF16_TFLOPS, 4),
+                "executed_flop_per_point": exec_pt, "algorithmic_flop_per_point": flop_per_point,
+                "layer_achieved": round(layer_tflops, 2), "layer_frac": round(layer_tflops / PEAK_BF16_TFLOPS, 4),
+                "layer_executed_frac": round(layer_exec / PEAK_BF16_TFLOPS, 4)}
 
     result = {
         "metric": METRIC, "value": N / (ms * 1e-3), "unit": "points/s", "n_gpus": 1,

@@ -118,11 +118,12 @@ typedef struct {
 
 /* Which buffer ts3_state_get / ts3_state_set address (float32, row-major). */
 typedef enum {
-    TS3_S_RAW = 0, /* [H, M, C]  sum_i w_i x_i            (valid after finalize) */
+    TS3_S_RAW = 0, /* [H, M, C]  sum_i w_i x_i            (valid after finalize; unprojected states) */
     TS3_D = 1,     /* [H, M]     sum_i w_i                (valid after finalize) */
     TS3_S = 2,     /* [H, M, dh] Linear1(d^-1 s_raw)      (valid after finalize) */
     TS3_S1 = 3,    /* [H, M, dh] Attention(s)             (valid after attention) */
-    TS3_ZP = 4     /* [H, M, C]  Linear3(s'), the cache   (valid after attention) */
+    TS3_ZP = 4,    /* [H, M, C]  Linear3(s'), the cache   (valid after attention) */
+    TS3_T_RAW = 5  /* [H, M, dh] sum_i w_i (x_i W1_h)     (valid after finalize; projected states) */
 } ts3_buffer;
 
 /* Allocate a state for one layer (device memory on the current HIP device) and
@@ -134,6 +135,17 @@ ts3_status ts3_state_free(ts3_state *st);
 
 /* Device bytes the state holds (for peak-memory reports). */
 ts3_status ts3_state_bytes(const ts3_state *st, int64_t *bytes);
+
+/* Whether the state accumulates projected sums (*projected = 1) or raw ones (0).
+ * Eq. (2) applies Linear1 to each point before the slice sum and the form of
+ * Eq. (4) after it; by linearity, sum_i w_i (x_i W1_h) = (sum_i w_i x_i) W1_h,
+ * so both give the same s.  Where it needs fewer products per point (bfloat16
+ * storage, C = 128, head width 16, M a multiple of 32) pass 1 sums the
+ * projected rows: each span partial row is then [dh + 1] floats (t, then the
+ * weight sum) instead of [C + 1], s_raw is not formed (TS3_S_RAW is
+ * UNSUPPORTED; TS3_T_RAW holds the projected sums), and accumulate also needs
+ * W1 (recorded at the first accumulate after reset, like W2/b2). */
+ts3_status ts3_state_projected(const ts3_state *st, int32_t *projected);
 
 /* Begin a new mesh: forget every accumulated tile.  Enqueues nothing. */
 ts3_status ts3_state_reset(ts3_state *st, void *stream);
@@ -236,8 +248,10 @@ ts3_status ts3_state_get(const ts3_state *st, int32_t which, float *host_dst, in
  * are the per-span terms of Eq. (4) before the ordered fold (finalize sums them
  * in span order).  Every requested span must have been accumulated since the
  * last reset, and no backward may have run since (it reuses the buffer):
- * otherwise TS3_ERR_BAD_STATE.  n must equal nspan*H*M*(C+1).  For tests and
- * inspection. */
+ * otherwise TS3_ERR_BAD_STATE.  n must equal nspan*H*M*(C+1).  A projected
+ * state (ts3_state_projected) holds [nspan][H][M][dh+1] instead: columns
+ * 0..dh-1 the span's sum of w_i (x_i W1_h), column dh the sum of w_i.  For
+ * tests and inspection. */
 ts3_status ts3_state_get_spans(const ts3_state *st, int64_t span0, int64_t nspan, float *host_dst, int64_t n,
                                void *stream);
 

@@ -12,7 +12,7 @@ from .build import LIB
 
 TS3_OK, TS3_ERR_INVALID_ARG, TS3_ERR_BAD_STATE, TS3_ERR_OUT_OF_MEMORY, TS3_ERR_HIP, TS3_ERR_UNSUPPORTED = range(6)
 TS3_FP32, TS3_BF16 = 0, 1
-TS3_S_RAW, TS3_D, TS3_S, TS3_S1, TS3_ZP = range(5)
+TS3_S_RAW, TS3_D, TS3_S, TS3_S1, TS3_ZP, TS3_T_RAW = range(6)
 
 
 TS3_ACCUM_FP32, TS3_ACCUM_FP64 = 0, 1
@@ -49,6 +49,7 @@ SIGNATURES = {
     "ts3_state_create": (ct.c_int, [ct.POINTER(Desc), ct.POINTER(_P)]),
     "ts3_state_free": (ct.c_int, [_P]),
     "ts3_state_bytes": (ct.c_int, [_P, ct.POINTER(ct.c_int64)]),
+    "ts3_state_projected": (ct.c_int, [_P, ct.POINTER(ct.c_int32)]),
     "ts3_state_reset": (ct.c_int, [_P, _P]),
     "ts3_slice_accumulate": (ct.c_int, [_P, ct.POINTER(Weights), _P, ct.c_int64, ct.c_int64, _P]),
     "ts3_slice_finalize": (ct.c_int, [_P, ct.POINTER(Weights), _P]),

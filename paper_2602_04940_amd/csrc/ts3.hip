@@ -17,6 +17,7 @@
 #include "ts3_pass1.h"
 #include "ts3_pass1pc.h"
 #include "ts3_pass1pcw.h"
+#include "ts3_pass1pcp.h"
 #include "ts3_pass2pc.h"
 #include "ts3_backward.h"
 #include "ts3_pass2.h"
@@ -76,6 +77,10 @@ struct Kernels {
                   hipStream_t);
     void (*bw_dw2)(const float *, const float *, int64_t, int64_t, int32_t, int32_t, int32_t, float *,
                    hipStream_t);
+    // Pass 1 in the projected form (bfloat16, C = 128, head width 16): x, n,
+    // span0, Q, nspan, H, W2', b2', W1 fragments, partials [span][H][M][17].
+    void (*pass1p)(const void *, int64_t, int64_t, int32_t, int32_t, int32_t, const void *, const float *,
+                   const void *, float *, hipStream_t) = nullptr;
     // Pass 2 in the slice-state form (bfloat16, head width 16): x, n, W2', b2',
     // s'^T fragments, W3^T fragments, b3, out.  NULL where it does not apply.
     hipError_t (*pass2sf)(const void *, int64_t, const void *, const float *, const void *, const void *,
@@ -210,6 +215,13 @@ void launch_bw_dx(const float *x, const float *g, int64_t n, int32_t H, const fl
 }
 
 template <int C, int M>
+void launch_pass1p(const void *x, int64_t n, int64_t span0, int32_t Q, int32_t nspan, int32_t H, const void *w2p,
+                   const float *b2s, const void *w1p, float *partials, hipStream_t st) {
+    hipLaunchKernelGGL((k_slice_accumulate_pcp<C, M>), dim3(nspan * (H / 2)), dim3(512), 0, st, (const bf16_t *)x,
+                       n, span0, Q, nspan, H, (const bf16_t *)w2p, b2s, (const bf16_t *)w1p, partials);
+}
+
+template <int C, int M>
 hipError_t launch_pass2sf(const void *x, int64_t n, const void *w2p, const float *b2s, const void *sf,
                           const void *w3f, const float *b3, void *out, hipStream_t st) {
     using Cfg = Pass2SFCfg<C, M>;
@@ -235,8 +247,11 @@ template <typename T, int C, int M> Kernels make_kernels() {
     else if constexpr (sizeof(T) == 4)
         return Kernels{&launch_pass1<T, C, M>, &launch_pass2<T, C, M>, &launch_bw_head<C, M>, &launch_bw_dx<C, M>,
                        &launch_bw_dw2<C, M>};
-    else if constexpr (C <= 128 && M % 32 == 0)
+    else if constexpr (C == 128 && M % 32 == 0)
         return Kernels{&launch_pass1<T, C, M>, &launch_pass2<T, C, M>, nullptr, nullptr, nullptr,
+                       &launch_pass1p<C, M>, &launch_pass2sf<C, M>};
+    else if constexpr (C <= 128 && M % 32 == 0)
+        return Kernels{&launch_pass1<T, C, M>, &launch_pass2<T, C, M>, nullptr, nullptr, nullptr, nullptr,
                        &launch_pass2sf<C, M>};
     else
         return Kernels{&launch_pass1<T, C, M>, &launch_pass2<T, C, M>, nullptr, nullptr, nullptr};
@@ -337,7 +352,12 @@ struct ts3_state {
     int phase = PH_RESET;
     bool w2_ready = false;
     bool partials_fwd = false;  // the partial buffer holds pass-1 span sums (not a backward's)
-    const float *W2 = nullptr, *b2 = nullptr;
+    const float *W2 = nullptr, *b2 = nullptr, *W1 = nullptr;
+    // projected pass 1 (k.pass1p and head width 16): the partials and the
+    // folded sums hold t = sum w (x W1) ([H][M][16]) instead of s_raw = sum w x
+    bool proj = false;
+    int rowc = 0;  // columns of a partial row before its d entry: dh if proj, else C
+    void *w1p = nullptr;
     // Second stream for ts3_layer_forward (default priority): consecutive
     // tiles and chunks alternate between it and the caller's stream, so one
     // launch's last partial round of workgroups overlaps the next launch's
@@ -405,6 +425,13 @@ ts3_status prep_w2(ts3_state *st, const ts3_weights *w, hipStream_t stream) {
         hipLaunchKernelGGL(k_prep_w2<float>, dim3(grid2), dim3(256), 0, stream, w->W2, w->b2, scale, d.C,
                            d.H, d.M, (float *)st->w2p, st->b2s);
     LAUNCH_CHECK("prep_w2");
+    if (st->proj && w->W1) {  // the W1 fragments of the projected pass 1
+        const int64_t nw1 = (int64_t)d.C * d.C;
+        hipLaunchKernelGGL(k_prep_w1, dim3((unsigned)std::min<int64_t>((nw1 + 255) / 256, 1024)), dim3(256), 0,
+                           stream, w->W1, d.C, d.H, (bf16_t *)st->w1p);
+        LAUNCH_CHECK("prep_w1");
+        st->W1 = w->W1;
+    }
     st->W2 = w->W2;
     st->b2 = w->b2;
     st->w2_ready = true;
@@ -456,7 +483,7 @@ ts3_status ts3_state_free(ts3_state *st) {
     hipError_t e = hipDeviceSynchronize();
     void *bufs[] = {st->partials, st->runs, st->s_raw, st->dsum, st->s,    st->s1,    st->Z,
                     st->b2s,      st->b3,   st->w2p,   st->zp,   st->bdZ,  st->bdsr,  st->bdsT,
-                    st->bdd,      st->bdW2T, st->bdz,  st->sfp,  st->w3p};
+                    st->bdd,      st->bdW2T, st->bdz,  st->sfp,  st->w3p,   st->w1p};
     for (void *b : bufs)
         if (b) (void)hipFree(b);
     if (st->ev_fork) (void)hipEventDestroy(st->ev_fork);
@@ -490,7 +517,9 @@ ts3_status ts3_state_create(const ts3_desc *desc, ts3_state **out) {
     const ts3_desc &d = st->desc;
     st->esize = d.io_dtype == TS3_BF16 ? 2 : 4;
     st->nspan_max = std::max<int64_t>(1, (d.max_points + d.group_span - 1) / d.group_span);
-    st->E = (int64_t)d.H * d.M * (d.C + 1);
+    st->proj = st->k.pass1p && d.H * 16 == d.C;
+    st->rowc = st->proj ? 16 : d.C;
+    st->E = (int64_t)d.H * d.M * (st->rowc + 1);
     st->nrun_max = (st->nspan_max + FOLD - 1) / FOLD;
     const int64_t HM = (int64_t)d.H * d.M;
     struct Req {
@@ -516,6 +545,7 @@ ts3_status ts3_state_create(const ts3_desc *desc, ts3_state **out) {
         // slice-state pass 2 (head width 16 only; empty otherwise)
         {&st->sfp, d.H * 16 == d.C && st->k.pass2sf ? HM * 16 * 2 : 0},
         {&st->w3p, d.H * 16 == d.C && st->k.pass2sf ? (int64_t)d.C * d.C * 2 : 0},
+        {&st->w1p, st->proj ? (int64_t)d.C * d.C * 4 : 0},  // W1 fragments [2][H][C/32][64][8]
     };
     if (d.H * 16 != d.C) st->k.pass2sf = nullptr;
     for (auto &r : reqs) {
@@ -576,8 +606,11 @@ ts3_status ts3_slice_accumulate(ts3_state *st, const ts3_weights *w, const void 
     if (point_offset + n_tile > d.max_points)
         return fail(TS3_ERR_INVALID_ARG, "tile end %lld exceeds max_points %lld",
                     (long long)(point_offset + n_tile), (long long)d.max_points);
+    if (st->proj && !w->W1) return fail(TS3_ERR_INVALID_ARG, "W1 is NULL (this layer accumulates projected sums)");
     if (st->w2_ready && !same_w2(st, w))
         return fail(TS3_ERR_INVALID_ARG, "W2/b2 differ from the ones recorded at the first accumulate");
+    if (st->w2_ready && st->proj && w->W1 != st->W1)
+        return fail(TS3_ERR_INVALID_ARG, "W1 differs from the one recorded at the first accumulate");
     const int64_t span0 = point_offset / Q;
     const int64_t nspan = (n_tile + Q - 1) / Q;
     const bool ragged = n_tile % Q != 0;
@@ -595,7 +628,11 @@ ts3_status ts3_slice_accumulate(ts3_state *st, const ts3_weights *w, const void 
         s = prep_w2(st, w, hs);
         if (s != TS3_OK) return s;
     }
-    st->k.pass1(x_tile, n_tile, span0, (int32_t)Q, (int32_t)nspan, d.H, d.C, d.M, st->w2p, st->b2s, st->partials,
+    if (st->proj)
+        st->k.pass1p(x_tile, n_tile, span0, (int32_t)Q, (int32_t)nspan, d.H, st->w2p, st->b2s, st->w1p, st->partials,
+                     hs);
+    else
+        st->k.pass1(x_tile, n_tile, span0, (int32_t)Q, (int32_t)nspan, d.H, d.C, d.M, st->w2p, st->b2s, st->partials,
                 hs);
     LAUNCH_CHECK("slice_accumulate");
     for (int64_t i = span0; i < span0 + nspan; ++i) st->span_written[(size_t)i] = 1;
@@ -613,21 +650,22 @@ namespace {
 // Ordered fold of the first nspan span partials into main [H*M*C] and the
 // column C entries into col [H*M] (the forward's fold kernels).
 template <typename T>
-ts3_status fold_partials_t(ts3_state *st, int64_t nspan, float *main, float *col, hipStream_t hs) {
-    const int64_t E = st->E;
+ts3_status fold_partials_t(ts3_state *st, int64_t nspan, int rowc, float *main, float *col, hipStream_t hs) {
+    const int64_t E = (int64_t)st->desc.H * st->desc.M * (rowc + 1);
     const int64_t nrun = (nspan + FOLD - 1) / FOLD;
     const unsigned gx = (unsigned)((E + 255) / 256);
     T *runs = reinterpret_cast<T *>(st->runs);
     hipLaunchKernelGGL(k_fold_runs<T>, dim3(gx, (unsigned)nrun), dim3(256), 0, hs, st->partials, E, nspan, runs);
     LAUNCH_CHECK("fold_runs");
-    hipLaunchKernelGGL(k_fold_final<T>, dim3(gx), dim3(256), 0, hs, runs, E, nrun, st->desc.C, main, col);
+    hipLaunchKernelGGL(k_fold_final<T>, dim3(gx), dim3(256), 0, hs, runs, E, nrun, rowc, main, col);
     LAUNCH_CHECK("fold_final");
     return TS3_OK;
 }
 
-ts3_status fold_partials(ts3_state *st, int64_t nspan, float *main, float *col, hipStream_t hs) {
-    return st->desc.accum == TS3_ACCUM_FP64 ? fold_partials_t<double>(st, nspan, main, col, hs)
-                                            : fold_partials_t<float>(st, nspan, main, col, hs);
+// rowc: columns of a partial row before its last (d-like) entry.
+ts3_status fold_partials(ts3_state *st, int64_t nspan, int rowc, float *main, float *col, hipStream_t hs) {
+    return st->desc.accum == TS3_ACCUM_FP64 ? fold_partials_t<double>(st, nspan, rowc, main, col, hs)
+                                            : fold_partials_t<float>(st, nspan, rowc, main, col, hs);
 }
 
 }  // namespace
@@ -654,10 +692,14 @@ ts3_status ts3_slice_finalize(ts3_state *st, const ts3_weights *w, void *stream)
         LAUNCH_CHECK("zero spans");
         i = j;
     }
-    const ts3_status s = fold_partials(st, nspan, st->s_raw, st->dsum, hs);
+    const ts3_status s = fold_partials(st, nspan, st->rowc, st->s_raw, st->dsum, hs);
     if (s != TS3_OK) return s;
-    hipLaunchKernelGGL(k_finalize, dim3(d.H), dim3(256), 0, hs, st->s_raw, st->dsum, w->W1, w->b1, d.C, d.H,
-                       d.M, d.dh, d.eps, st->s);
+    if (st->proj)
+        hipLaunchKernelGGL(k_finalize_proj, dim3(d.H), dim3(256), 0, hs, st->s_raw, st->dsum, w->b1, d.H, d.M, d.eps,
+                           st->s);
+    else
+        hipLaunchKernelGGL(k_finalize, dim3(d.H), dim3(256), 0, hs, st->s_raw, st->dsum, w->W1, w->b1, d.C, d.H,
+                           d.M, d.dh, d.eps, st->s);
     LAUNCH_CHECK("finalize");
     st->phase = PH_FINAL;
     return TS3_OK;
@@ -839,7 +881,7 @@ ts3_status ts3_layer_backward(ts3_state *st, const ts3_weights *w, const void *x
                       st->b2s, st->partials, hs);
         LAUNCH_CHECK("backward dZ pass");
     }
-    ts3_status s = fold_partials(st, nspan_all, st->bdZ, st->bdd, hs);
+    ts3_status s = fold_partials(st, nspan_all, d.C, st->bdZ, st->bdd, hs);
     if (s != TS3_OK) return s;
     // token side: ds_raw, dd and the Linear1 / attention / Linear3 gradients
     const size_t lds = (size_t)(2 * d.M * d.C + 10 * d.M * d.dh + 2 * d.M * d.M) * 4;
@@ -860,11 +902,17 @@ ts3_status ts3_layer_backward(ts3_state *st, const ts3_weights *w, const void *x
                      st->partials, hs);
         LAUNCH_CHECK("backward dW2 pass");
     }
-    s = fold_partials(st, nspan_all, st->bdW2T, gr->db2, hs);
+    s = fold_partials(st, nspan_all, d.C, st->bdW2T, gr->db2, hs);
     if (s != TS3_OK) return s;
     hipLaunchKernelGGL(k_bw_transpose_w2, dim3((unsigned)std::min<int64_t>((d.C * HM + 255) / 256, 4096)), dim3(256),
                        0, hs, st->bdW2T, d.C, (int)HM, gr->dW2);
     LAUNCH_CHECK("dW2 transpose");
+    return TS3_OK;
+}
+
+ts3_status ts3_state_projected(const ts3_state *st, int32_t *projected) {
+    if (!st || !projected) return fail(TS3_ERR_INVALID_ARG, "NULL argument");
+    *projected = st->proj ? 1 : 0;
     return TS3_OK;
 }
 
@@ -876,7 +924,16 @@ ts3_status ts3_state_get(const ts3_state *st, int32_t which, float *host_dst, in
     int64_t size = 0;
     int need = PH_FINAL;
     switch (which) {
-        case TS3_S_RAW: src = st->s_raw; size = HM * d.C; break;
+        case TS3_S_RAW:
+            if (st->proj) return fail(TS3_ERR_UNSUPPORTED, "this state accumulates projected sums: read TS3_T_RAW");
+            src = st->s_raw;
+            size = HM * d.C;
+            break;
+        case TS3_T_RAW:
+            if (!st->proj) return fail(TS3_ERR_UNSUPPORTED, "this state accumulates unprojected sums: read TS3_S_RAW");
+            src = st->s_raw;
+            size = HM * 16;
+            break;
         case TS3_D: src = st->dsum; size = HM; break;
         case TS3_S: src = st->s; size = HM * d.dh; break;
         case TS3_S1: src = st->s1; size = HM * d.dh; need = PH_ATTEND; break;
@@ -971,13 +1028,16 @@ ts3_status scratch_base(void **out) {
 
 // Byte layout of the scratch array for one call (each region 256-aligned).
 struct ScratchLayout {
-    size_t partials, runs, s_raw, dsum, s, s1, Z, b2s, b3, w2p, zp, sfp, w3p, total;
+    size_t partials, runs, s_raw, dsum, s, s1, Z, b2s, b3, w2p, zp, sfp, w3p, w1p, total;
 };
 
 ScratchLayout scratch_layout(const ts3_desc &d, int64_t N, int64_t tile) {
     auto up = [](size_t b) { return (b + 255) & ~size_t(255); };
     const int64_t HM = (int64_t)d.H * d.M;
-    const int64_t E = HM * (d.C + 1);
+    Kernels k;
+    find_any_kernels(d.io_dtype, d.C, d.M, &k);
+    const bool proj = k.pass1p && d.H * 16 == d.C;  // the projected pass 1, as for a state
+    const int64_t E = HM * ((proj ? 16 : d.C) + 1);
     const int64_t Q = d.group_span;
     const int64_t tile_spans = (std::min<int64_t>(tile, std::max<int64_t>(N, 1)) + Q - 1) / Q;
     // An empty mesh still folds one (zero) span.
@@ -995,13 +1055,12 @@ ScratchLayout scratch_layout(const ts3_desc &d, int64_t N, int64_t tile) {
     take(L.Z, (size_t)(HM * d.C) * 4);
     take(L.b2s, (size_t)HM * 4);
     take(L.b3, (size_t)d.C * 4);
-    Kernels k;
-    find_any_kernels(d.io_dtype, d.C, d.M, &k);
     take(L.w2p, (size_t)w2p_elems(d) * esize);
     take(L.zp, (size_t)zp_elems(d, k.rt) * esize);
     const bool sf = k.pass2sf && d.H * 16 == d.C;  // the slice-state pass 2, as for a state
     take(L.sfp, sf ? (size_t)HM * 16 * 2 : 0);
     take(L.w3p, sf ? (size_t)d.C * d.C * 2 : 0);
+    take(L.w1p, proj ? (size_t)d.C * d.C * 4 : 0);
     L.total = at;
     return L;
 }
@@ -1052,7 +1111,10 @@ ts3_status ts3_layer_forward_noalloc(const ts3_desc *desc, const ts3_weights *w,
     st.desc = d;
     find_any_kernels(d.io_dtype, d.C, d.M, &st.k);
     st.esize = d.io_dtype == TS3_BF16 ? 2 : 4;
-    st.E = (int64_t)d.H * d.M * (d.C + 1);
+    st.proj = st.k.pass1p && d.H * 16 == d.C;
+    st.rowc = st.proj ? 16 : d.C;
+    st.E = (int64_t)d.H * d.M * (st.rowc + 1);
+    st.w1p = st.proj ? b + lay.w1p : nullptr;
     st.partials = (float *)(b + lay.partials);
     st.runs = (float *)(b + lay.runs);
     st.s_raw = (float *)(b + lay.s_raw);
@@ -1089,8 +1151,12 @@ ts3_status ts3_layer_forward_noalloc(const ts3_desc *desc, const ts3_weights *w,
     for (int64_t t0 = 0; t0 < N; t0 += tile) {
         const int64_t nt = std::min(tile, N - t0);
         const int64_t ns = (nt + Q - 1) / Q;
-        st.k.pass1((const char *)x + t0 * d.C * st.esize, nt, 0, (int32_t)Q, (int32_t)ns, d.H, d.C, d.M, st.w2p,
-                   st.b2s, st.partials, hs);
+        if (st.proj)
+            st.k.pass1p((const char *)x + t0 * d.C * st.esize, nt, 0, (int32_t)Q, (int32_t)ns, d.H, st.w2p, st.b2s,
+                        st.w1p, st.partials, hs);
+        else
+            st.k.pass1((const char *)x + t0 * d.C * st.esize, nt, 0, (int32_t)Q, (int32_t)ns, d.H, d.C, d.M,
+                       st.w2p, st.b2s, st.partials, hs);
         LAUNCH_CHECK("slice_accumulate");
         if (d.accum == TS3_ACCUM_FP64) fold_tile<double>(st.partials, E, t0 / Q, ns, st.runs, hs);
         else fold_tile<float>(st.partials, E, t0 / Q, ns, st.runs, hs);
@@ -1098,14 +1164,18 @@ ts3_status ts3_layer_forward_noalloc(const ts3_desc *desc, const ts3_weights *w,
     }
     const unsigned gx = (unsigned)((E + 255) / 256);
     if (d.accum == TS3_ACCUM_FP64)
-        hipLaunchKernelGGL(k_fold_final<double>, dim3(gx), dim3(256), 0, hs, (const double *)st.runs, E, nrun, d.C,
-                           st.s_raw, st.dsum);
+        hipLaunchKernelGGL(k_fold_final<double>, dim3(gx), dim3(256), 0, hs, (const double *)st.runs, E, nrun,
+                           st.rowc, st.s_raw, st.dsum);
     else
-        hipLaunchKernelGGL(k_fold_final<float>, dim3(gx), dim3(256), 0, hs, (const float *)st.runs, E, nrun, d.C,
-                           st.s_raw, st.dsum);
+        hipLaunchKernelGGL(k_fold_final<float>, dim3(gx), dim3(256), 0, hs, (const float *)st.runs, E, nrun,
+                           st.rowc, st.s_raw, st.dsum);
     LAUNCH_CHECK("fold_final");
-    hipLaunchKernelGGL(k_finalize, dim3(d.H), dim3(256), 0, hs, st.s_raw, st.dsum, w->W1,
-                       w->b1, d.C, d.H, d.M, d.dh, d.eps, st.s);
+    if (st.proj)
+        hipLaunchKernelGGL(k_finalize_proj, dim3(d.H), dim3(256), 0, hs, st.s_raw, st.dsum, w->b1, d.H, d.M, d.eps,
+                           st.s);
+    else
+        hipLaunchKernelGGL(k_finalize, dim3(d.H), dim3(256), 0, hs, st.s_raw, st.dsum, w->W1, w->b1, d.C, d.H, d.M,
+                           d.dh, d.eps, st.s);
     LAUNCH_CHECK("finalize");
     st.phase = PH_FINAL;
     s = ts3_token_attention(&st, w, stream);

@@ -140,6 +140,20 @@ __global__ void k_finalize(const float *__restrict__ s_raw, const float *__restr
     }
 }
 
+// Projected form (head width 16): t_raw [H][M][16] already holds
+// sum_i w_i (x_i W1_h), so s = t_raw / (d + eps) + b1, zero mean for an
+// empty slice as above.
+__global__ void k_finalize_proj(const float *__restrict__ t_raw, const float *__restrict__ dsum,
+                                const float *__restrict__ b1, int H, int M, float eps, float *__restrict__ s) {
+    const int h = blockIdx.x;
+    for (int i = threadIdx.x; i < M * 16; i += blockDim.x) {
+        const int m = i >> 4, col = h * 16 + (i & 15);
+        const float den = dsum[h * M + m] + eps;
+        const float v = t_raw[((int64_t)h * M + m) * 16 + (i & 15)];
+        s[((int64_t)h * M + m) * 16 + (i & 15)] = (den > 0.f ? v / den : 0.f) + (b1 ? b1[col] : 0.f);
+    }
+}
+
 // Per-head attention among the M slice tokens, then Linear3 without bias:
 // q,k,v = s Wq[h], s Wk[h], s Wv[h]; A = softmax(q k^T / sqrt(dh)); s1 = A v;
 // Z[h][m][c] = s1[m][:] . W3[h*dh .. h*dh+dh-1][c].  One workgroup per head.

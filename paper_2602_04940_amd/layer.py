@@ -88,6 +88,12 @@ class PhysicsAttention:
         L.check(L.lib().ts3_state_bytes(self.h, ct.byref(b)), "ts3_state_bytes")
         return b.value
 
+    def projected(self) -> bool:
+        """True when pass 1 sums x_i W1_h per head (rows of dh + 1) instead of x_i."""
+        v = ct.c_int32()
+        L.check(L.lib().ts3_state_projected(self.h, ct.byref(v)), "ts3_state_projected")
+        return bool(v.value)
+
     # ----------------------------------------------------------- ABI calls
     def reset(self):
         L.check(L.lib().ts3_state_reset(self.h, _stream()), "ts3_state_reset")
@@ -145,15 +151,16 @@ class PhysicsAttention:
     def get(self, which: int) -> np.ndarray:
         H, M, C, dh = self.H, self.M, self.C, self.dh
         shape = {L.TS3_S_RAW: (H, M, C), L.TS3_D: (H, M), L.TS3_S: (H, M, dh), L.TS3_S1: (H, M, dh),
-                 L.TS3_ZP: (H, M, C)}[which]
+                 L.TS3_ZP: (H, M, C), L.TS3_T_RAW: (H, M, dh)}[which]
         a = np.empty(shape, dtype=np.float32)
         L.check(L.lib().ts3_state_get(self.h, which, a.ctypes.data_as(ct.c_void_p), a.size, _stream()),
                 "ts3_state_get")
         return a
 
     def get_spans(self, span0: int, nspan: int) -> np.ndarray:
-        """Span partials [nspan, H, M, C+1] (columns :C sum w x, column C sum w)."""
-        a = np.empty((nspan, self.H, self.M, self.C + 1), dtype=np.float32)
+        """Span partials [nspan, H, M, C+1] (columns :C sum w x, column C sum w),
+        or [nspan, H, M, dh+1] (sum w x W1_h, then sum w) for a projected state."""
+        a = np.empty((nspan, self.H, self.M, (self.dh if self.projected() else self.C) + 1), dtype=np.float32)
         L.check(L.lib().ts3_state_get_spans(self.h, span0, nspan, a.ctypes.data_as(ct.c_void_p), a.size,
                                             _stream()), "ts3_state_get_spans")
         return a

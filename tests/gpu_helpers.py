@@ -71,10 +71,11 @@ def assert_bf16_close(got, ref, what, tol=2e-2, block=256):
 
 
 def assert_state_close(st, ref, what, tol=2e-2):
-    """bf16-path state against the oracle: s_raw and Z per slice token (rows of
-    [H*M, C]), d element by element, each within the bf16 bar."""
+    """bf16-path state against the oracle: the slice sums (s_raw [H, M, C] or
+    the projected t_raw [H, M, dh]) and Z per slice token, d element by
+    element, each within the bf16 bar."""
     H, M = np.asarray(ref["d"]).shape
-    for k in ("s_raw", "Z"):
+    for k in ("s_raw", "t_raw", "Z"):
         if k in st:
             assert_bf16_close(np.asarray(st[k]).reshape(H * M, -1), np.asarray(ref[k]).reshape(H * M, -1),
                               f"{what} {k}", tol, block=M)
@@ -83,3 +84,36 @@ def assert_state_close(st, ref, what, tol=2e-2):
     ed = float((np.abs(dg - dr) / np.maximum(np.abs(dr), 1e-300)).max()) if dr.size else 0.0
     print(f"{what} d: worst element rel {ed:.3e}", flush=True)
     assert ed <= tol, (what, "d", ed)
+
+
+def sums_key(st):
+    """'t_raw' for a state that sums projected rows (x_i W1_h per head), else 's_raw'."""
+    return "t_raw" if "t_raw" in st else "s_raw"
+
+
+def state_of(layer):
+    """The layer's state buffers as float32 host arrays: d, s, s1, Z and the
+    slice sums in the form the state keeps them (s_raw or t_raw)."""
+    from paper_2602_04940_amd import _lib as L
+    st = {"d": layer.get(L.TS3_D), "s": layer.get(L.TS3_S), "s1": layer.get(L.TS3_S1), "Z": layer.get(L.TS3_ZP)}
+    if layer.projected():
+        st["t_raw"] = layer.get(L.TS3_T_RAW)
+    else:
+        st["s_raw"] = layer.get(L.TS3_S_RAW)
+    return st
+
+
+def match_sums(st, ref_st, x, W, H, M, inv_tau, tile=None):
+    """Give the oracle state the sums the GPU state holds: for a projected
+    state, t_raw from oracle.projected_accumulate over consecutive tiles of
+    `tile` points (the whole mesh at once when tile is None)."""
+    if "t_raw" in st and "t_raw" not in ref_st:
+        import oracle
+        N = len(x)
+        step = tile or max(N, 1)
+        dh = W["W1"].shape[1] // H
+        t = np.zeros((H, M, dh))
+        for i in range(0, N, step):
+            t += oracle.projected_accumulate(x[i:i + step], W["W2"], W["b2"], W["W1"], H, M, inv_tau)[0]
+        ref_st["t_raw"] = t
+    return ref_st

@@ -52,6 +52,41 @@ def test_fp64_fold_matches_oracle_and_is_tiling_independent():
         assert max(e) <= 1e-4
 
 
+def test_fp64_fold_of_projected_sums_bf16():
+    """bfloat16 storage at C = 128, head width 16: the span partials hold
+    projected rows (dh + 1 floats); the float64 fold of them matches the
+    oracle's projected sums and is bitwise independent of the tiling."""
+    import torch
+    from paper_2602_04940_amd import LayerWeights, _lib as L
+    from gpu_helpers import assert_bf16_close, assert_state_close, match_sums
+    from ts3_synth import round_bf16
+    C, H, M, N, Q = 128, 8, 64, 70_000, 512
+    banner(f"fp64 fold of projected sums, bf16 storage, N={N}, Q={Q}")
+    rng = np.random.default_rng(6)
+    x64 = round_bf16(rng.standard_normal((N, C)))
+    W = make_weights(C, H, M, C // H, seed=2, bias_seed=3)
+    x = to_device(x64, "bf16")
+    lw = LayerWeights(W)
+    got = {}
+    for accum, tile in (("fp64", 8192), ("fp64", N + 512 - N % 512), ("fp32", 8192)):
+        with _layer(C, H, M, Q, N + 512, accum, "bf16") as layer:
+            assert layer.projected()
+            out = layer.forward(lw, x, tile=tile, chunk=8192)
+            torch.cuda.synchronize()
+            got[(accum, tile)] = (to_host(out), layer.get(L.TS3_T_RAW), layer.get(L.TS3_D), layer.get(L.TS3_ZP))
+    a, b = got[("fp64", 8192)], got[("fp64", N + 512 - N % 512)]
+    assert all(np.array_equal(u, v) for u, v in zip(a, b))
+    it = 2.0
+    st = oracle.build_state(x64, W, H, M, it, tile=N)
+    ref_out = oracle.deslice(x64, W["W2"], W["b2"], st["Z"], W["b3"], H, M, it)
+    for accum in ("fp64", "fp32"):
+        out, t_raw, d, Z = got[(accum, 8192)]
+        g = {"t_raw": t_raw, "d": d, "Z": Z}
+        match_sums(g, st, x64, W, H, M, it)
+        assert_state_close(g, st, f"{accum} fold state", 2e-2)
+        assert_bf16_close(out, ref_out, f"{accum} fold out", 2e-2)
+
+
 def test_fold_drift_on_a_160m_point_mesh():
     import torch
     from paper_2602_04940_amd import LayerWeights, _lib as L

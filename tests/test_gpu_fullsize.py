@@ -11,7 +11,8 @@ that hold at any size:
   * the state equals the index-ordered sum of all 6,400 span partials, within
     the rounding bound of float32 addition in runs of 64 and then 100 (the
     fold of Eq. (4));
-  * sum_m d[h, m] = N and sum_m s_raw[h, m, :] = sum_i x_i for every head;
+  * sum_m d[h, m] = N and sum_m s_raw[h, m, :] = sum_i x_i for every head
+    (for a state of projected sums, sum_m t_raw[h, m, :] = (sum_i x_i) W1_h);
   * reruns, and 10M-point tiles, give bitwise equal states and outputs.
 Pass 2 over the whole mesh decodes an injected random state, checked against
 the oracle on 64 seeded whole 256-row blocks and 4,096 seeded points, per row,
@@ -64,7 +65,10 @@ def test_pass1_spans_fold_invariants_tiling_and_determinism_at_100m(mesh):
     out = torch.empty_like(x)
     with _layer(wl) as layer:
         layer.forward(lw, x, tile=wl.tile, chunk=wl.chunk, out=out)
-        s_raw, d, Z = layer.get(L.TS3_S_RAW).astype(np.float64), layer.get(L.TS3_D).astype(np.float64), layer.get(L.TS3_ZP)
+        proj = layer.projected()
+        key = L.TS3_T_RAW if proj else L.TS3_S_RAW
+        R = wl.dh if proj else C  # columns of a sums row before its weight sum
+        s_raw, d, Z = layer.get(key).astype(np.float64), layer.get(L.TS3_D).astype(np.float64), layer.get(L.TS3_ZP)
         banner(f"all {nspan} span partials")
         parts = layer.get_spans(0, nspan)
         first = out.clone()
@@ -73,7 +77,7 @@ def test_pass1_spans_fold_invariants_tiling_and_determinism_at_100m(mesh):
         assert np.array_equal(layer.get(L.TS3_ZP), Z)
         assert torch.equal(out, first)
         layer.forward(lw, x, tile=10 * wl.tile, chunk=wl.chunk, out=out)
-        assert np.array_equal(layer.get(L.TS3_S_RAW).astype(np.float64), s_raw)
+        assert np.array_equal(layer.get(key).astype(np.float64), s_raw)
         assert np.array_equal(layer.get(L.TS3_ZP), Z)
         assert torch.equal(out, first)
         del first
@@ -82,11 +86,13 @@ def test_pass1_spans_fold_invariants_tiling_and_determinism_at_100m(mesh):
     spans = np.sort(np.random.default_rng(50).choice(nspan, N_SPANS_SAMPLED, replace=False))
     banner(f"oracle sums over spans {spans.tolist()}")
     xs = [to_host(x[j * Q:(j + 1) * Q]) for j in spans]
+    name = "t_raw" if proj else "s_raw"
     with OraclePool(min(N_SPANS_SAMPLED, 16)) as pool:
-        refs = pool.sums(xs, W["W2"], W["b2"], H, M, 1.0 / wl.tau)
+        refs = (pool.projected_sums(xs, W["W2"], W["b2"], W["W1"], H, M, 1.0 / wl.tau) if proj else
+                pool.sums(xs, W["W2"], W["b2"], H, M, 1.0 / wl.tau))
     for j, (sr, dj) in zip(spans, refs):
         p = parts[j]
-        assert_state_close({"s_raw": p[:, :, :C], "d": p[:, :, C]}, {"s_raw": sr, "d": dj}, f"span {j}", BF16_TOL)
+        assert_state_close({name: p[:, :, :R], "d": p[:, :, R]}, {name: sr, "d": dj}, f"span {j}", BF16_TOL)
 
     # The fold: float32 sums of 64 consecutive spans, then of the 100 run sums,
     # in index order.  Each element's error is at most (63 + 99) * 2^-24 times
@@ -106,6 +112,9 @@ def test_pass1_spans_fold_invariants_tiling_and_determinism_at_100m(mesh):
     # well under 1e-5 relative.
     np.testing.assert_allclose(d.sum(axis=1), N, rtol=2.0 ** -9 + 1e-5)
     # sum_m s_raw[h, m, c] - sum_i x_ic = sum_i eps_i x_ic with |eps_i| <= 2^-9.
+    # Projected sums: sum_m t_raw[h, m, j] - (sum_i x_i W1_h)_j also carries the
+    # bfloat16 rounding of W1 and of each point's projected row (2^-9 each,
+    # relative to sum_c |x_ic W1_cj|): at most (2^-8 + 1e-5) (sum_i |x_i|) |W1_h|.
     colsum = np.zeros(C)
     abssum = np.zeros(C)
     for c0 in range(0, N, wl.chunk):
@@ -113,8 +122,14 @@ def test_pass1_spans_fold_invariants_tiling_and_determinism_at_100m(mesh):
         colsum += xc.sum(dim=0).cpu().numpy()
         abssum += xc.abs().sum(dim=0).cpu().numpy()
     for h in range(H):
-        err = np.abs(s_raw[h].sum(axis=0) - colsum)
-        assert (err <= (2.0 ** -9 + 1e-5) * abssum).all(), (h, (err / abssum).max())
+        if proj:
+            W1h = W["W1"][:, h * wl.dh:(h + 1) * wl.dh].astype(np.float64)
+            err = np.abs(s_raw[h].sum(axis=0) - colsum @ W1h)
+            lim = (2.0 ** -8 + 1e-5) * (abssum @ np.abs(W1h))
+        else:
+            err = np.abs(s_raw[h].sum(axis=0) - colsum)
+            lim = (2.0 ** -9 + 1e-5) * abssum
+        assert (err <= lim).all(), (h, (err / lim).max())
 
 
 def test_pass2_on_injected_state_at_100m_sampled(mesh):

@@ -10,7 +10,8 @@ own through ts3_layer_forward with the benchmark's kernels and launch shape.
 That is one pass-1 launch over 64 spans of 15,625 points (489 blocks per span)
 and one pass-2 launch of 256 persistent workgroups.  Checked against the
 oracle (Eq. (1), (3)-(5), Algorithm 1):
-  * the state: s_raw and Z per slice token, d per element;
+  * the state: the slice sums (s_raw, or t_raw for a state of projected sums)
+    and Z per slice token, d per element;
   * the output: every row, each 256-row block, and the whole window.
 With random-init weights the token attention nearly averages each head's
 tokens, so all output rows are close to one vector, and the output check alone
@@ -61,11 +62,16 @@ def test_window_state_and_output_at_the_bench_launch(window, pool):
                           max_points=CHUNK) as layer:
         out = layer.forward(lw, x, tile=wl.tile, chunk=wl.chunk)
         torch.cuda.synchronize()
-        st = {"s_raw": layer.get(L.TS3_S_RAW), "d": layer.get(L.TS3_D), "Z": layer.get(L.TS3_ZP)}
+        proj = layer.projected()
+        st = {"d": layer.get(L.TS3_D), "Z": layer.get(L.TS3_ZP)}
+        st["t_raw" if proj else "s_raw"] = layer.get(L.TS3_T_RAW if proj else L.TS3_S_RAW)
     got = to_host(out)
     banner(f"oracle on window {k} ({pool.workers} host processes)")
     it = 1.0 / wl.tau
     ref_st = pool.state(x64, W, wl.H, wl.M, it)
+    if proj:
+        parts = pool.projected_tile_sums(x64, W["W2"], W["b2"], W["W1"], wl.H, wl.M, it, 65536)
+        ref_st["t_raw"] = sum((t[0] for t in parts), np.zeros((wl.H, wl.M, wl.dh)))
     ref = pool.decode(x64, W["W2"], W["b2"], ref_st["Z"], W["b3"], wl.H, wl.M, it)
     assert_state_close(st, ref_st, "state", BF16_TOL)
     assert_bf16_close(got, ref, "out", BF16_TOL)

@@ -10,7 +10,8 @@ import numpy as np
 import pytest
 
 import oracle
-from gpu_helpers import assert_bf16_close, assert_state_close, banner, normwise, rel_l2, to_device, to_host
+from gpu_helpers import (assert_bf16_close, assert_state_close, banner, match_sums, normwise, rel_l2, state_of,
+                         sums_key, to_device, to_host)
 from ts3_synth import WORKLOADS, make_weights
 from ts3_synth.workloads import small_features
 
@@ -36,9 +37,7 @@ def _weights(W):
 
 
 def _state(layer):
-    from paper_2602_04940_amd import _lib as L
-    return {"s_raw": layer.get(L.TS3_S_RAW), "d": layer.get(L.TS3_D), "s": layer.get(L.TS3_S),
-            "s1": layer.get(L.TS3_S1), "Z": layer.get(L.TS3_ZP)}
+    return state_of(layer)
 
 
 def _run(x64, W, C, H, M, dtype, tau, tile, chunk, Q, eps=0.0):
@@ -59,8 +58,8 @@ def test_fp32_ellipsoid_4k_layer_and_state():
     x = small_features(wl, wl.N)
     W = make_weights(wl.C, wl.H, wl.M, wl.dh, seed=0)
     got, st, _ = _run(x, W, wl.C, wl.H, wl.M, "fp32", wl.tau, tile=wl.tile, chunk=wl.chunk, Q=1024)
-    ref_st = oracle.build_state(x, W, wl.H, wl.M, 1 / wl.tau)
-    for k in ("s_raw", "d", "s", "s1", "Z"):
+    ref_st = match_sums(st, oracle.build_state(x, W, wl.H, wl.M, 1 / wl.tau), x, W, wl.H, wl.M, 1 / wl.tau)
+    for k in (sums_key(st), "d", "s", "s1", "Z"):
         assert normwise(st[k], ref_st[k]) <= FP32_TOL, k
     ref = oracle.layer_forward_fast(x, W, wl.H, wl.M, 1 / wl.tau)
     err = normwise(got, ref)
@@ -87,11 +86,12 @@ def test_bf16_ellipsoid_1m_tiled_matches_oracle_and_untiled_bitwise(ellipsoid_1m
     wl, x, W, ref, ref_st = ellipsoid_1m
     banner(f"{wl.name}: N={wl.N} tile={wl.tile} Q={wl.group_span} bf16")
     got, st, out_t = _run(x, W, wl.C, wl.H, wl.M, "bf16", wl.tau, wl.tile, wl.chunk, wl.group_span)
+    match_sums(st, ref_st, x, W, wl.H, wl.M, 1 / wl.tau, wl.tile)
     assert_bf16_close(got, ref, "out", BF16_TOL)
     assert_state_close(st, ref_st, "state", BF16_TOL)
     one_tile = -(-wl.N // wl.group_span) * wl.group_span
     got1, st1, out_1 = _run(x, W, wl.C, wl.H, wl.M, "bf16", wl.tau, one_tile, wl.N, wl.group_span)
-    assert np.array_equal(st1["Z"], st["Z"]) and np.array_equal(st1["s_raw"], st["s_raw"])
+    assert np.array_equal(st1["Z"], st["Z"]) and np.array_equal(st1[sums_key(st)], st[sums_key(st)])
     assert torch.equal(out_1, out_t)
 
 
@@ -116,10 +116,10 @@ def test_shapes_ragged_tiles_random_biases(C, H, M, dtype):
     W = make_weights(C, H, M, C // H, seed=3, bias_seed=4)
     got, st, _ = _run(x, W, C, H, M, dtype, 0.5, tile, chunk, Q)
     ref = oracle.layer_forward_fast(x, W, H, M, 2.0)
-    ref_st = oracle.build_state(x, W, H, M, 2.0)
+    ref_st = match_sums(st, oracle.build_state(x, W, H, M, 2.0), x, W, H, M, 2.0)
     if dtype == "fp32":
         assert normwise(got, ref) <= FP32_TOL
-        for k in ("s_raw", "d", "Z"):
+        for k in (sums_key(st), "d", "Z"):
             assert normwise(st[k], ref_st[k]) <= FP32_TOL, k
     else:
         assert_bf16_close(got, ref, "out", BF16_TOL)
@@ -139,12 +139,12 @@ def test_wide_rows_bf16_ragged_spans_random_biases(C, H, M):
     W = make_weights(C, H, M, C // H, seed=3, bias_seed=4)
     got, st, _ = _run(x, W, C, H, M, "bf16", 0.5, tile, chunk, Q)
     ref = oracle.layer_forward_fast(x, W, H, M, 2.0)
-    ref_st = oracle.build_state(x, W, H, M, 2.0)
+    ref_st = match_sums(st, oracle.build_state(x, W, H, M, 2.0), x, W, H, M, 2.0)
     assert_bf16_close(got, ref, "out", BF16_TOL)
     assert_state_close(st, ref_st, "state", BF16_TOL)
     got1, st1, _ = _run(x, W, C, H, M, "bf16", 0.5, 2304, N, Q)
     assert np.array_equal(got1, got)
-    for k in ("s_raw", "d", "Z"):
+    for k in (sums_key(st), "d", "Z"):
         assert np.array_equal(st1[k], st[k]), k
 
 
@@ -169,17 +169,17 @@ def test_runtime_shape_kernels_ragged_tiles(C, H, M, dtype):
     W = make_weights(C, H, M, C // H, seed=5, bias_seed=6)
     got, st, _ = _run(x, W, C, H, M, dtype, 0.5, tile, chunk, Q)
     ref = oracle.layer_forward_fast(x, W, H, M, 2.0)
-    ref_st = oracle.build_state(x, W, H, M, 2.0)
+    ref_st = match_sums(st, oracle.build_state(x, W, H, M, 2.0), x, W, H, M, 2.0)
     if dtype == "fp32":
         assert normwise(got, ref) <= FP32_TOL
-        for k in ("s_raw", "d", "Z"):
+        for k in (sums_key(st), "d", "Z"):
             assert normwise(st[k], ref_st[k]) <= FP32_TOL, k
     else:
         assert_bf16_close(got, ref, "out", BF16_TOL)
         assert_state_close(st, ref_st, "state", BF16_TOL)
     got1, st1, _ = _run(x, W, C, H, M, dtype, 0.5, 1120, N, Q)
     assert np.array_equal(got1, got)
-    for k in ("s_raw", "d", "Z"):
+    for k in (sums_key(st), "d", "Z"):
         assert np.array_equal(st1[k], st[k]), k
 
 
@@ -197,12 +197,12 @@ def test_bf16_two_head_workgroups_odd_block_counts(Q):
     W = make_weights(C, H, M, C // H, seed=7, bias_seed=8)
     got, st, out_t = _run(x, W, C, H, M, "bf16", 0.5, 10 * Q, 1000, Q)
     ref = oracle.layer_forward_fast(x, W, H, M, 2.0)
-    ref_st = oracle.build_state(x, W, H, M, 2.0)
+    ref_st = match_sums(st, oracle.build_state(x, W, H, M, 2.0), x, W, H, M, 2.0)
     assert_bf16_close(got, ref, "out", BF16_TOL)
     assert_state_close(st, ref_st, "state", BF16_TOL)
     one_tile = -(-N // Q) * Q
     got1, st1, out_1 = _run(x, W, C, H, M, "bf16", 0.5, one_tile, N, Q)
-    for k in ("s_raw", "d", "Z"):
+    for k in (sums_key(st), "d", "Z"):
         assert np.array_equal(st1[k], st[k]), k
     assert np.array_equal(got1, got)
 
@@ -238,7 +238,7 @@ def test_one_hot_slices_fp32():
     assert len(x) == N
     got, st, _ = _run(x, W, C, H, M, "fp32", 1.0 / 200.0, 512, 512, 256)
     ref_st = oracle.build_state(x, W, H, M, 200.0)
-    assert normwise(st["s_raw"], ref_st["s_raw"]) <= FP32_TOL
+    assert normwise(st[sums_key(st)], ref_st[sums_key(st)]) <= FP32_TOL
     assert normwise(st["d"], ref_st["d"]) <= FP32_TOL
     ref = oracle.layer_forward_fast(x, W, H, M, 200.0)
     assert normwise(got, ref) <= FP32_TOL
@@ -274,7 +274,7 @@ def test_bf16_shifted_softmax_fallback_mixed_with_fast_path(C, Q):
     assert np.abs(lg[:lo]).max() < 40 and np.abs(lg[hi:]).max() < 40   # fast-path rows elsewhere
     got, st, _ = _run(x, W, C, H, M, "bf16", 1 / it, 3 * Q if C == 128 else 4 * Q, 1000, Q)
     ref = oracle.layer_forward_fast(x, W, H, M, it)
-    ref_st = oracle.build_state(x, W, H, M, it)
+    ref_st = match_sums(st, oracle.build_state(x, W, H, M, it), x, W, H, M, it)
     assert_bf16_close(got, ref, "out", BF16_TOL)
     assert_state_close(st, ref_st, "state", BF16_TOL)
 
@@ -412,3 +412,22 @@ def test_call_order_and_argument_errors():
     with pytest.raises(L.TS3Error) as e:
         PhysicsAttention(C, H, M, C // H, 0.5, "fp32", group_span=32, max_points=10 ** 9)  # ~0.5 TB
     assert e.value.status == L.TS3_ERR_OUT_OF_MEMORY
+
+
+def test_projected_state_reports_its_sums():
+    """bfloat16 storage, C = 128, head width 16, M a multiple of 32: pass 1
+    sums projected rows and the state exposes t_raw, not s_raw; float32
+    storage and wider heads keep the unprojected sums."""
+    from paper_2602_04940_amd import _lib as L
+    banner("projected-state buffers")
+    for (C, H, M, dtype, proj) in [(128, 8, 64, "bf16", True), (128, 8, 32, "bf16", True),
+                                   (128, 8, 64, "fp32", False), (128, 2, 64, "bf16", False),
+                                   (128, 8, 16, "bf16", False), (64, 4, 32, "bf16", False)]:
+        with _layer(C, H, M, dtype, Q=128, max_points=256) as layer:
+            assert layer.projected() == proj, (C, H, M, dtype)
+            hidden = L.TS3_S_RAW if proj else L.TS3_T_RAW
+            try:
+                layer.get(hidden)
+                raise AssertionError("no error")
+            except L.TS3Error as e:
+                assert e.status == L.TS3_ERR_UNSUPPORTED, (C, H, M, dtype, e.status)
