@@ -308,7 +308,8 @@ def summarize_traffic(fetch_dir: str, write_dir: str, command: str):
                                                   "bytes_per_counted_byte": factor}
         for kname in ("k_slice_accumulate_pc", "k_slice_accumulate_pcp", "k_deslice_w8", "k_deslice_sf"):
             vals = [float(r["Counter_Value"]) for r in rs if kname + "<" in r["Kernel_Name"]]
-            per.setdefault(kname, {})[name] = (sum(vals) / len(vals), len(vals), factor)
+            if vals:  # kernels the workload did not run are left out
+                per.setdefault(kname, {})[name] = (sum(vals) / len(vals), len(vals), factor)
     for kname, d in per.items():
         f_kib, n, f_fac = d["FETCH_SIZE"]
         w_kib, _, w_fac = d["WRITE_SIZE"]
