@@ -431,3 +431,44 @@ def test_projected_state_reports_its_sums():
                 raise AssertionError("no error")
             except L.TS3Error as e:
                 assert e.status == L.TS3_ERR_UNSUPPORTED, (C, H, M, dtype, e.status)
+
+
+@pytest.mark.parametrize("dtype,eps", [("fp32", 0.0), ("fp32", 0.5), ("bf16", 0.0), ("bf16", 0.5)])
+def test_empty_slices_and_eps(dtype, eps):
+    """One-hot slice weights (1/tau = 20000, every point's top two logits at
+    least 0.05 apart in every head, so the other weights underflow to zero in
+    float32 and float64 alike), and every fourth slice's bias lowered by 5 so
+    that no point reaches it: those slices have d = 0 and s = b1 exactly
+    (reading 7); eps > 0 divides by d + eps.  bf16 at C = 128 with head width
+    16 runs the projected pass 1; both passes take the shifted softmax (the
+    exp2 sums overflow)."""
+    C, H, M, N = 128, 8, 64, 1500
+    banner(f"empty slices, eps={eps}, {dtype}")
+    rng = np.random.default_rng(61)
+    from ts3_synth import round_storage
+    W = make_weights(C, H, M, C // H, seed=21, bias_seed=22)
+    b2 = W["b2"].copy().reshape(H, M)
+    b2[:, ::4] -= 5.0
+    W["b2"] = b2.reshape(-1)
+    cand = round_storage(rng.standard_normal((8 * N, C)), dtype)
+    lg = np.sort((cand @ W["W2"].astype(np.float64) + W["b2"]).reshape(-1, H, M), axis=2)
+    x = cand[((lg[:, :, -1] - lg[:, :, -2]) > 0.05).all(axis=1)][:N]
+    assert len(x) == N
+    it = 20000.0
+    got, st, _ = _run(x, W, C, H, M, dtype, 1.0 / it, 512, 700, 256, eps=eps)
+    ref_st = match_sums(st, oracle.build_state(x, W, H, M, it, eps=eps), x, W, H, M, it)
+    ref = oracle.layer_forward_fast(x, W, H, M, it, eps=eps)
+    empty = ref_st["d"] == 0
+    print(f"{int(empty.sum())} of {H * M} slices empty", flush=True)
+    assert empty.sum() >= 8 and (~empty).sum() >= 8
+    assert (st["d"][empty] == 0).all()
+    b1 = W["b1"].astype(np.float32).reshape(H, 1, C // H)
+    assert np.array_equal(st["s"][empty], np.broadcast_to(b1, st["s"].shape)[empty])
+    if dtype == "fp32":
+        for k in (sums_key(st), "d", "s", "Z"):
+            assert normwise(st[k], ref_st[k]) <= FP32_TOL, k
+        assert normwise(got, ref) <= FP32_TOL
+    else:
+        assert_state_close(st, ref_st, "state", BF16_TOL)
+        assert_bf16_close(st["s"].reshape(H * M, -1), ref_st["s"].reshape(H * M, -1), "state s", BF16_TOL, block=M)
+        assert_bf16_close(got, ref, "out", BF16_TOL)

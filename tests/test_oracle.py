@@ -122,6 +122,30 @@ def test_projected_sums_are_additive_and_empty_slices_give_b1():
     np.testing.assert_array_equal(s, np.broadcast_to(W["b1"].astype(np.float64).reshape(4, 1, 4), s.shape))
 
 
+def test_projected_state_equals_raw_state_with_eps_and_empty_slices():
+    """Reading 1's order with eps > 0 and with slices that no point reaches:
+    the projected state t / (d + eps) + b1 equals Linear1((d + eps)^-1 s_raw)
+    + b1, and an empty slice (d + eps = 0) gives b1 in both."""
+    x, W = _rand_case(N=200, C=12, H=3, M=5, seed=17)
+    s_raw, d = oracle.slice_accumulate(x, W["W2"], W["b2"], 3, 5, 1.3)
+    t, d2 = oracle.projected_accumulate(x, W["W2"], W["b2"], W["W1"], 3, 5, 1.3)
+    np.testing.assert_array_equal(d, d2)
+    for eps in (0.0, 0.25, 7.0):
+        np.testing.assert_allclose(oracle.projected_finalize(t, d, W["b1"], 3, eps),
+                                   oracle.slice_finalize(s_raw, d, W["W1"], W["b1"], 3, eps), rtol=0, atol=1e-12)
+    empty = np.zeros_like(d, dtype=bool)
+    empty[0, 1] = empty[2, 4] = True
+    s_raw[empty] = 0
+    t[empty] = 0
+    d = np.where(empty, 0.0, d)
+    sp = oracle.projected_finalize(t, d, W["b1"], 3)
+    sr = oracle.slice_finalize(s_raw, d, W["W1"], W["b1"], 3)
+    np.testing.assert_allclose(sp, sr, rtol=0, atol=1e-12)
+    b1 = W["b1"].astype(np.float64).reshape(3, 4)
+    np.testing.assert_array_equal(sp[0, 1], b1[0])
+    np.testing.assert_array_equal(sp[2, 4], b1[2])
+
+
 # ------------------------------------------------------ invariants of Eq. (1)
 
 def test_softmax_rows_sum_to_one_and_d_sums_to_N():
