@@ -13,9 +13,9 @@
 //                   by 64 hidden units: [F/64][W_a^T part | W_b part], 64*C
 //                   elements each, so one linear copy stages a chunk.
 //   k_mlp_residual_pc  one kernel for the rest of the block: y = x + PA
-//                   output, LN2, both feed-forward products with the exact GELU
-//                   between them, the residual, and optionally the next
-//                   block's LN1.
+//                   output, LN2, both feed-forward products with GELU (its
+//                   tanh form in half precision, gelu2_f16) between them, the
+//                   residual, and optionally the next block's LN1.
 //
 // k_mlp_residual_pc: 128 points per workgroup, 32 per pair of waves sharing a
 // SIMD.  The producer keeps LN2(y) of its points as B fragments (K = channels)
@@ -38,42 +38,25 @@ namespace ts3 {
 
 constexpr float BLOCK_LN_EPS = 1e-5f;
 
-// GELU(x) = x Phi(x) of two values, evaluated on packed halves.  Phi by
-// Abramowitz & Stegun, formula 26.2.17 (|error| < 7.5e-8 in exact
-// arithmetic): with t = 1 / (1 + 0.2316419 |x|) and
-// h = exp(-x^2 / 2) (c1 t + ... + c5 t^5), c_k = b_k / sqrt(2 pi), the lower
-// tail Phi(-|x|) is h, so Phi(x) = h for x < 0 and 1 - h for x >= 0; taking
-// the tail directly avoids the cancellation of 1 + erf at negative x.  In
-// half precision (every operation rounded to f16) the RMS relative error over
-// N(0, 1.5^2) inputs is 1.2e-3, as large as rounding the exact value to bf16
-// (the hidden activations' former storage); the worst relative error is 1e-2
-// where |GELU| is near 1e-3, and the worst absolute error 4e-3 is the f16
-// rounding of x near 8.  Pre-activations beyond the f16 range (65504) would
-// overflow; LayerNorm'd inputs through a 4C-wide layer stay orders of
-// magnitude below it.  Returns the pair as the f16 B-operand slots of the
-// second product.
+// GELU(x) = x Phi(x) of two values, evaluated on packed halves with the
+// tanh form of Hendrycks and Gimpel: Phi(x) ~ (1 + tanh(sqrt(2/pi) (x +
+// 0.044715 x^3))) / 2 = 1 / (1 + exp(-2 sqrt(2/pi) (x + 0.044715 x^3))), so
+// GELU(x) ~ x / (1 + 2^u) with u = -x (K1 + K2 x^2), K1 = 2 sqrt(2/pi) / ln 2,
+// K2 = 0.044715 K1: four packed operations, two exp2 and two reciprocals per
+// pair.  The form differs from x Phi(x) by at most 4.7e-4 (absolute); in half
+// precision (every operation rounded to f16) the RMS absolute error over
+// N(0, 1.5^2) inputs is 4.7e-4 and the worst 3.8e-3 (the f16 rounding of x near
+// 8).  The tails need no care: for very negative x, 2^u overflows to infinity
+// and the reciprocal gives 0; for large x, 2^u underflows and GELU(x) = x.
+// Returns the pair as the f16 B-operand slots of the second product.
 __device__ __forceinline__ f16x2 gelu2_f16(float a, float b) {
     const f16x2 x{(_Float16)a, (_Float16)b};
-    const f16x2 ax = __builtin_elementwise_abs(x);
-    const f16x2 den = ax * (_Float16)0.2316419f + (_Float16)1.0f;
-    f16x2 t;
-    t[0] = __builtin_amdgcn_rcph(den[0]);
-    t[1] = __builtin_amdgcn_rcph(den[1]);
-    f16x2 p = t * (_Float16)0.5307027145f + (_Float16)-0.7265760136f;
-    p = p * t + (_Float16)0.7107068703f;
-    p = p * t + (_Float16)-0.1422483683f;
-    p = p * t + (_Float16)0.1274147958f;
-    p = p * t;
-    const f16x2 h = p * __builtin_elementwise_exp2(x * x * (_Float16)-0.7213475204f);  // exp(-x^2/2)
-    const f16x2 up = (_Float16)1.0f - h;
-    uint32_t m, phi;
-    // m: each half all ones where x < 0 (both halves shifted by 15: the count
-    // comes from a register, since an inline constant would reach the high
-    // half as zero); phi = x < 0 ? h : 1 - h, half by half
-    asm("v_pk_ashrrev_i16 %0, %1, %2" : "=v"(m) : "s"(0x000F000Fu), "v"(__builtin_bit_cast(uint32_t, x)));
-    asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(phi)
-        : "v"(m), "v"(__builtin_bit_cast(uint32_t, h)), "v"(__builtin_bit_cast(uint32_t, up)));
-    return x * __builtin_bit_cast(f16x2, phi);
+    const f16x2 u = x * ((x * x) * (_Float16)-0.10294280f + (_Float16)-2.30220819f);
+    const f16x2 d = __builtin_elementwise_exp2(u) + (_Float16)1.0f;
+    f16x2 r;
+    r[0] = __builtin_amdgcn_rcph(d[0]);
+    r[1] = __builtin_amdgcn_rcph(d[1]);
+    return x * r;
 }
 
 __device__ __forceinline__ void unpack8(const uint4 &u, float (&v)[8]) {
