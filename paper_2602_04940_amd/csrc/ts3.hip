@@ -217,7 +217,7 @@ void launch_bw_dx(const float *x, const float *g, int64_t n, int32_t H, const fl
 template <int C, int M>
 void launch_pass1p(const void *x, int64_t n, int64_t span0, int32_t Q, int32_t nspan, int32_t H, const void *w2p,
                    const float *b2s, const void *w1p, float *partials, hipStream_t st) {
-    hipLaunchKernelGGL((k_slice_accumulate_pcp<C, M>), dim3(nspan * (H / 2)), dim3(512), 0, st, (const bf16_t *)x,
+    hipLaunchKernelGGL((k_slice_accumulate_pcp<C, M>), dim3(nspan * (H / 2)), dim3(PCP_THREADS), 0, st, (const bf16_t *)x,
                        n, span0, Q, nspan, H, (const bf16_t *)w2p, b2s, (const bf16_t *)w1p, partials);
 }
 
