@@ -25,6 +25,7 @@ def test_committed_traffic_summary_matches_the_kernel_sources():
         t = json.load(f)
     if t["source_hash"] != bench.kernel_source_hash():
         pytest.skip("kernel sources changed since the counters were taken: bench.py reports traffic null")
-    for k in ("k_slice_accumulate_pc", "k_deslice_w8"):
+    # the two passes of the benchmark's layer (projected pass 1, slice-state pass 2)
+    for k in ("k_slice_accumulate_pcp", "k_deslice_sf"):
         assert t["kernels"][k]["points"] == 1_000_000
         assert bench.measured_traffic(k, 1_000_000) == t["kernels"][k]["hbm_bytes_per_launch"]
