@@ -183,12 +183,13 @@ def test_runtime_shape_kernels_ragged_tiles(C, H, M, dtype):
         assert np.array_equal(st1[k], st[k]), k
 
 
-@pytest.mark.parametrize("Q", [96, 100])
+@pytest.mark.parametrize("Q", [64, 96, 100, 160])
 def test_bf16_two_head_workgroups_odd_block_counts(Q):
-    """Pass 1 with two heads per workgroup: a span of Q = 96 points has three
-    32-point blocks, so the second block stream's last step has no points;
-    Q = 100 leaves it 4.  States match the oracle and tiled runs match an
-    untiled one bitwise."""
+    """Pass 1 with two heads per workgroup and the span's 32-point blocks in
+    three interleaved streams: Q = 64 gives two blocks (the third stream has
+    none), Q = 96 one block per stream, Q = 100 four blocks (the last of 4
+    points; two streams end on a step with no points), Q = 160 five blocks.
+    States match the oracle and tiled runs match an untiled one bitwise."""
     C, H, M, N = 128, 8, 64, 4100
     banner(f"two-head pass 1, Q={Q}, N={N}")
     rng = np.random.default_rng(Q)
