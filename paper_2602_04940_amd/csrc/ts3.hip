@@ -698,8 +698,8 @@ ts3_status ts3_slice_finalize(ts3_state *st, const ts3_weights *w, void *stream)
         hipLaunchKernelGGL(k_finalize_proj, dim3(d.H), dim3(256), 0, hs, st->s_raw, st->dsum, w->b1, d.H, d.M, d.eps,
                            st->s);
     else
-        hipLaunchKernelGGL(k_finalize, dim3(d.H), dim3(256), 0, hs, st->s_raw, st->dsum, w->W1, w->b1, d.C, d.H,
-                           d.M, d.dh, d.eps, st->s);
+        hipLaunchKernelGGL(k_finalize, dim3(d.H * d.M), dim3(64), 0, hs, st->s_raw, st->dsum, w->W1, w->b1, d.C,
+                           d.H, d.M, d.dh, d.eps, st->s);
     LAUNCH_CHECK("finalize");
     st->phase = PH_FINAL;
     return TS3_OK;
@@ -1174,8 +1174,8 @@ ts3_status ts3_layer_forward_noalloc(const ts3_desc *desc, const ts3_weights *w,
         hipLaunchKernelGGL(k_finalize_proj, dim3(d.H), dim3(256), 0, hs, st.s_raw, st.dsum, w->b1, d.H, d.M, d.eps,
                            st.s);
     else
-        hipLaunchKernelGGL(k_finalize, dim3(d.H), dim3(256), 0, hs, st.s_raw, st.dsum, w->W1, w->b1, d.C, d.H, d.M,
-                           d.dh, d.eps, st.s);
+        hipLaunchKernelGGL(k_finalize, dim3(d.H * d.M), dim3(64), 0, hs, st.s_raw, st.dsum, w->W1, w->b1, d.C, d.H,
+                           d.M, d.dh, d.eps, st.s);
     LAUNCH_CHECK("finalize");
     st.phase = PH_FINAL;
     s = ts3_token_attention(&st, w, stream);

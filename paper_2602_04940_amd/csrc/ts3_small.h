@@ -118,25 +118,28 @@ __global__ void k_fold_final(const T *__restrict__ runs, int64_t E, int64_t nrun
 }
 
 // s[h][m][j] = (d^-1 s_raw)[h][m][:] . W1[:, h*dh + j] + b1[h*dh + j]; one
-// workgroup per head.  The mean is taken before Linear1 (the physical state of
-// Appendix A.4); an empty slice (d + eps <= 0) has mean zero.  The mean is
-// formed where it is used (s_raw rows stay in L2), so no shape needs LDS.
+// workgroup of one wave per slice token (grid H*M), a lane per output column.
+// The mean is taken before Linear1 (the physical state of Appendix A.4); an
+// empty slice (d + eps <= 0) has mean zero.  The mean is formed where it is
+// used (s_raw rows stay in L2), so no shape needs LDS.  Each output is one
+// sequential sum over c, so the launch shape does not change its rounding.
 __global__ void k_finalize(const float *__restrict__ s_raw, const float *__restrict__ dsum,
                            const float *__restrict__ W1, const float *__restrict__ b1, int C, int H,
                            int M, int dh, float eps, float *__restrict__ s) {
-    const int h = blockIdx.x;
+    const int hm = blockIdx.x;  // h * M + m
+    const int h = hm / M;
     const int HD = H * dh;
-    for (int i = threadIdx.x; i < M * dh; i += blockDim.x) {
-        const int m = i / dh, jj = i - m * dh;
+    const float den = dsum[hm] + eps;
+    const float *row = s_raw + (int64_t)hm * C;
+    for (int jj = threadIdx.x; jj < dh; jj += blockDim.x) {
         const int col = h * dh + jj;
-        const float den = dsum[h * M + m] + eps;
-        const float *row = s_raw + ((int64_t)h * M + m) * C;
         float acc = b1 ? b1[col] : 0.f;
+#pragma unroll 8
         for (int c = 0; c < C; ++c) {
             const float mean = den > 0.f ? row[c] / den : 0.f;
             acc = fmaf(mean, W1[(int64_t)c * HD + col], acc);
         }
-        s[((int64_t)h * M + m) * dh + jj] = acc;
+        s[(int64_t)hm * dh + jj] = acc;
     }
 }
 
