@@ -716,7 +716,9 @@ ts3_status ts3_token_attention(ts3_state *st, const ts3_weights *w, void *stream
     if (lds > 64 * 1024)
         HIP_TRY(hipFuncSetAttribute((const void *)k_attention, hipFuncAttributeMaxDynamicSharedMemorySize,
                                     ATTN_LDS_MAX));
-    hipLaunchKernelGGL(k_attention, dim3(d.H), dim3(256), lds, hs, st->s, w->Wq, w->Wk, w->Wv, w->W3, d.C, d.H,
+    // Z's columns in blocks of 64 over as many workgroups per head
+    const int zb = d.C % 64 == 0 ? d.C / 64 : 1;
+    hipLaunchKernelGGL(k_attention, dim3(d.H, zb), dim3(256), lds, hs, st->s, w->Wq, w->Wk, w->Wv, w->W3, d.C, d.H,
                        d.M, d.dh, st->s1, st->Z);
     LAUNCH_CHECK("attention");
     if (w->b3)

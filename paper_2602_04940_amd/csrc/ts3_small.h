@@ -159,7 +159,9 @@ __global__ void k_finalize_proj(const float *__restrict__ t_raw, const float *__
 
 // Per-head attention among the M slice tokens, then Linear3 without bias:
 // q,k,v = s Wq[h], s Wk[h], s Wv[h]; A = softmax(q k^T / sqrt(dh)); s1 = A v;
-// Z[h][m][c] = s1[m][:] . W3[h*dh .. h*dh+dh-1][c].  One workgroup per head.
+// Z[h][m][c] = s1[m][:] . W3[h*dh .. h*dh+dh-1][c].  Grid (H, ZB): the ZB
+// workgroups of a head each run its attention (the same arithmetic, so the
+// same s1) and write Z for their C / ZB columns; the first also writes s1.
 __global__ void k_attention(const float *__restrict__ s, const float *__restrict__ Wq,
                             const float *__restrict__ Wk, const float *__restrict__ Wv,
                             const float *__restrict__ W3, int C, int H, int M, int dh,
@@ -214,11 +216,12 @@ __global__ void k_attention(const float *__restrict__ s, const float *__restrict
         float acc = 0.f;
         for (int b = 0; b < M; ++b) acc = fmaf(A[a * M + b], v[b * dh + jj], acc);
         o[i] = acc;
-        s1[(int64_t)h * n + i] = acc;
+        if (blockIdx.y == 0) s1[(int64_t)h * n + i] = acc;
     }
     __syncthreads();
-    for (int i = threadIdx.x; i < M * C; i += blockDim.x) {
-        const int m = i / C, c = i - m * C;
+    const int CB = C / (int)gridDim.y, c0 = (int)blockIdx.y * CB;
+    for (int i = threadIdx.x; i < M * CB; i += blockDim.x) {
+        const int m = i / CB, c = c0 + (i - m * CB);
         float acc = 0.f;
         for (int u = 0; u < dh; ++u) acc = fmaf(o[m * dh + u], W3[(int64_t)(h * dh + u) * C + c], acc);
         Z[((int64_t)h * M + m) * C + c] = acc;
